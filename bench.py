@@ -1,0 +1,222 @@
+#!/usr/bin/env python3
+"""One-GPU benchmark of the MI355X attention forward.
+
+A timed step is one call of the attention forward on the headline workload
+(default: GQA causal prefill, B=1, Hq=32, Hkv=8, Nq=Nk=2048, D=64, bf16) with
+its inputs already resident in HBM; the value is algorithmic TFLOP/s
+(4 * D FLOPs per visible query-key pair per head).  The decode path (split-KV
+plus log-sum-exp merge) is timed in the same run on the GQA decode workload
+(B=16, Hq=32, Hkv=8, Nk=8192, D=128, bf16) as KV-read GB/s, and the other
+workloads are reported alongside.  The fp64 CPU oracle is timed on the host
+cores on the headline workload as a baseline (not a target), and the GPU
+output of the benchmark is checked against it.
+
+Prints ONE JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_MFMA_TFLOPS = {"bf16": 2500.0, "f16": 2500.0, "f32": 157.3}   # dense, MI355X
+PEAK_HBM_GBS = 8000.0
+METRIC = "prefill attention TFLOP/s (% MFMA peak); decode KV GB/s (% HBM peak)"
+PREFILL_SOURCES = ["paper_2608_18656_amd/csrc/fa_prefill.hip",
+                   "paper_2608_18656_amd/csrc/fa_common.h"]
+DECODE_SOURCES = ["paper_2608_18656_amd/csrc/fa_decode.hip",
+                  "paper_2608_18656_amd/csrc/fa_common.h"]
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def source_hash(paths):
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def stored_traffic(kernel: str, workload: str, paths):
+    """HBM bytes per launch from the committed rocprofv3 counter runs, or None
+    when they were taken on a different version of the kernel source."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f).get(kernel, {}).get(workload)
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("source_sha256") != source_hash(paths):
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def time_calls(torch, fns, steps, warmup):
+    """Mean ms per call over ``steps`` back-to-back calls (cycling through
+    ``fns``), bracketed by device synchronisation; HIP events recorded on the
+    current stream, which is the stream the kernels are launched on."""
+    stream = torch.cuda.current_stream()
+    for i in range(warmup):
+        fns[i % len(fns)]()
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for i in range(steps):
+        fns[i % len(fns)]()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    return t0.elapsed_time(t1) / steps
+
+
+def run_workload(torch, fa, w, steps, warmup, kv_sets=1, num_splits=None):
+    from paper_2608_18656_amd.inputs import make_workload
+
+    q, k, v = make_workload(w)
+    sets = [(q.cuda(), k.cuda(), v.cuda())]
+    for extra in range(1, kv_sets):   # more K/V copies so every call streams from HBM
+        q2, k2, v2 = make_workload(w, seed=w.seed + 1000 * extra)
+        sets.append((q2.cuda(), k2.cuda(), v2.cuda()))
+    del q, k, v
+    outs = [torch.empty_like(s[0]) for s in sets]
+    lses = [torch.empty((w.B, w.Hq, w.Nq), dtype=torch.float32, device="cuda") for _ in sets]
+
+    def make(i):
+        qd, kd, vd = sets[i]
+        return lambda: fa.fwd(qd, kd, vd, causal=w.causal, scale=w.softmax_scale, out=outs[i],
+                              lse=lses[i], num_splits=num_splits)
+
+    ms = time_calls(torch, [make(i) for i in range(len(sets))], steps, warmup)
+    return ms, sets[0], outs[0], lses[0]
+
+
+def cpu_baseline(w, q_cpu_dev, o_dev, lse_dev):
+    """The oracle as it stands, on the host cores, over the whole workload;
+    also the max error of the benchmark's GPU output against it."""
+    import numpy as np
+
+    import oracle
+
+    q, k, v = (t.cpu() for t in q_cpu_dev)
+    stats = {}
+    t0 = time.perf_counter()
+    o_ref, l_ref = oracle.attention_parallel(q, k, v, w.causal, w.softmax_scale,
+                                             workers=oracle.default_workers(), stats=stats)
+    wall = time.perf_counter() - t0
+    og = oracle.to_f64(o_dev)
+    err = float(np.abs(og - o_ref).max())
+    lerr = float(np.abs(oracle.to_f64(lse_dev) - l_ref).max())
+    return ({"value": w.flops() / wall / 1e12, "unit": "TFLOP/s", "cores": stats["workers"],
+             "kind": "oracle", "cpu_seconds": round(stats["cpu_s"], 2),
+             "wall_seconds": round(wall, 2),
+             "sample": f"whole {w.name} workload ({w.B * w.Hq * w.Nq} query rows), fp64 C, "
+                       f"one thread per worker process"},
+            {"max_abs_err_vs_oracle": err, "lse_max_abs_err": lerr})
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="gqa_prefill_bf16")
+    ap.add_argument("--no-extras", action="store_true", help="headline workload only")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE "
+              f"{world}); this attention forward is built and measured on a single MI355X",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2608_18656_amd as fa
+    from paper_2608_18656_amd.inputs import WORKLOADS
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    w = WORKLOADS[args.workload]
+    decode_main = w.Nq == 1
+    log(f"[bench] headline {w.name}: steps {args.steps} warmup {args.warmup}")
+    ms, inputs, out, lse = run_workload(torch, fa, w, args.steps, args.warmup,
+                                        kv_sets=2 if decode_main else 1)
+    if decode_main:
+        value, unit = w.kv_bytes() / (ms * 1e-3) / 1e9, "GB/s"
+        peak, bound, runit = PEAK_HBM_GBS, "hbm", "GB/s"
+        algo = w.kv_bytes()
+        kname, ksrc = "decode_split_kernel", DECODE_SOURCES
+    else:
+        value, unit = w.flops() / (ms * 1e-3) / 1e12, "TFLOP/s"
+        peak, bound, runit = PEAK_MFMA_TFLOPS[w.dtype], "mfma", "TFLOP/s"
+        algo = w.flops()
+        kname, ksrc = "prefill_kernel", PREFILL_SOURCES
+    log(f"[bench] {w.name}: {ms * 1e3:.1f} us/call, {value:.1f} {unit}")
+    result = {
+        "metric": METRIC, "value": round(value, 3), "unit": unit, "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 6),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+        "data": "synthetic (seeded i.i.d. inputs shaped like the paper's SLM layers)",
+        "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "Nq": w.Nq,
+                   "Nk": w.Nk, "D": w.D, "causal": w.causal, "scale": w.softmax_scale,
+                   "parallelism": "single GPU"},
+        "roofline": {"bound": bound, "achieved": round(value, 3), "peak": peak, "unit": runit,
+                     "frac": round(value / peak, 4),
+                     "traffic": stored_traffic(kname, w.name, ksrc),
+                     "kernel": kname, "algorithmic_per_launch": algo,
+                     "launch_us": round(ms * 1e3, 3)},
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] cpu baseline: oracle on host cores")
+        base, parity = cpu_baseline(w, inputs, out, lse)
+        result["cpu_baseline"] = base
+        result["parity"] = parity
+        log(f"[bench] oracle {base['wall_seconds']} s wall on {base['cores']} cores; "
+            f"gpu max err {parity['max_abs_err_vs_oracle']:.3e}")
+    del inputs, out, lse
+    torch.cuda.empty_cache()
+
+    if not args.no_extras:
+        extras = []
+        for name in ("gqa_decode_bf16", "mqa_decode_f16", "gqa_prefill_d128_f16",
+                     "mqa_prefill_f16", "gqa_prefill_bf16", "tiny_mha_f32"):
+            if name == w.name:
+                continue
+            x = WORKLOADS[name]
+            steps = max(5, min(args.steps, 30))
+            xms, *_ = run_workload(torch, fa, x, steps, 3, kv_sets=2 if x.Nq == 1 else 1)
+            if x.Nq == 1:
+                val, u, pk = x.kv_bytes() / (xms * 1e-3) / 1e9, "GB/s", PEAK_HBM_GBS
+            else:
+                val, u = x.flops() / (xms * 1e-3) / 1e12, "TFLOP/s"
+                pk = PEAK_MFMA_TFLOPS[x.dtype]
+            extras.append({"workload": name, "us_per_call": round(xms * 1e3, 2),
+                           "value": round(val, 2), "unit": u, "frac": round(val / pk, 4),
+                           "steps": steps})
+            log(f"[bench] {name}: {xms * 1e3:.1f} us/call, {val:.1f} {u} ({100 * val / pk:.1f}%)")
+            torch.cuda.empty_cache()
+        # achievable HBM bandwidth for context: a plain 1 GiB device copy
+        src = torch.empty(1 << 29, dtype=torch.float16, device="cuda").fill_(1.0)
+        dst = torch.empty_like(src)
+        cms = time_calls(torch, [lambda: dst.copy_(src)], 20, 3)
+        extras.append({"workload": "device_copy_1GiB", "us_per_call": round(cms * 1e3, 2),
+                       "value": round(2 * src.numel() * 2 / (cms * 1e-3) / 1e9, 1),
+                       "unit": "GB/s (read + write)"})
+        result["workloads"] = extras
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

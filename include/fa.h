@@ -1,0 +1,132 @@
+/*
+ * fa.h -- C ABI of the MI355X (gfx950) FlashAttention forward library.
+ *
+ * Computes exact softmax attention, o = softmax(scale * q k^T) v, per query
+ * head (the scaled dot-product definition of Sec. 2), for multi-head,
+ * grouped-query and multi-query attention (Sec. 1; Sec. 4.1.1: a key/value
+ * row is shared by the query heads of its group), in prefill (many query
+ * rows) and decode (one query row against a long key/value cache, Sec. 4.1:
+ * "(1 x D)" operands).  The result is reached with the streaming softmax of
+ * Alg. 1 carried over key blocks as in Alg. 2 (running row maximum, running
+ * row sum, rescaled accumulator, one final 1/l normalisation); decode splits
+ * the key range over workgroups and merges the partial results by their
+ * log-sum-exp.
+ *
+ * Tensors (all dense, row-major, D fastest, device memory owned by the
+ * caller):
+ *   q   [B][Nq][Hq][D]    element type = in_dtype          read only
+ *   k   [B][Nk][Hkv][D]   element type = in_dtype          read only
+ *   v   [B][Nk][Hkv][D]   element type = in_dtype          read only
+ *   o   [B][Nq][Hq][D]    element type = out_dtype         written
+ *   lse [B][Hq][Nq]       float32, may be NULL (then not written)
+ *                         lse = ln(sum over visible keys of exp(scale*q.k))
+ *
+ * Head map: query head h reads key/value head h / (Hq / Hkv) (contiguous
+ * groups); Hq must be a multiple of Hkv.
+ * Causal mask (bottom-right): key j is visible to query row i iff
+ * j <= i + (Nk - Nq).  With Nq == Nk this is the usual lower triangle; with
+ * Nq == 1 every key is visible.  causal with Nq > Nk is rejected (it would
+ * leave rows with no visible key).
+ * Precision: fp16 / bf16 inputs use fp32 accumulation and fp32 softmax state;
+ * the probabilities enter the second product as fp16 (bf16 values are
+ * converted to fp16 there, exact for |v| <= 65504 and within 2^-25 absolute
+ * below 2^-14).  fp32 inputs are computed in fp32 throughout.  Outputs are
+ * rounded to nearest even.
+ *
+ * Calls enqueue work on `stream` (a hipStream_t; NULL = the null stream) and
+ * return without synchronising.  Argument errors are reported synchronously,
+ * before any HIP call; device faults surface at the caller's next
+ * synchronisation.  No exception crosses this interface.
+ *
+ * Decode needs a device workspace for the per-split partial results.  The
+ * library owns one per device, grows it on demand (hipMalloc, which may
+ * synchronise) and keeps it until fa_release_workspace(); make one warm-up
+ * call before timing.  Calls on the same device share that workspace, so
+ * concurrent calls on different streams of one device race: serialise them.
+ */
+#ifndef FA_H_
+#define FA_H_
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    FA_F16 = 0,  /* IEEE binary16 */
+    FA_BF16 = 1, /* bfloat16 */
+    FA_F32 = 2   /* IEEE binary32 */
+} fa_dtype_t;
+
+typedef enum {
+    FA_OK = 0,
+    FA_ERR_NULL = 1,         /* q, k, v or o is NULL */
+    FA_ERR_DIM = 2,          /* a size is < 1, or an index would overflow int64 */
+    FA_ERR_GQA_RATIO = 3,    /* Hq is not a multiple of Hkv */
+    FA_ERR_HEAD_DIM = 4,     /* D unsupported: D % 8 != 0 or D > 256 */
+    FA_ERR_CAUSAL_SHAPE = 5, /* causal with Nq > Nk */
+    FA_ERR_SCALE = 6,        /* scale is NaN or infinite */
+    FA_ERR_ALIGN = 7,        /* a tensor pointer is not 16-byte aligned */
+    FA_ERR_ALIAS = 8,        /* o or lse overlaps q, k, v, or each other */
+    FA_ERR_DTYPE = 9,        /* unknown dtype, or out_dtype not in {in_dtype, FA_F32} */
+    FA_ERR_WORKSPACE = 10,   /* workspace allocation failed */
+    FA_ERR_HIP = 11,         /* a HIP runtime call or kernel launch failed */
+    FA_ERR_SPLITS = 12       /* num_splits outside [0, FA_MAX_SPLITS] */
+} fa_status_t;
+
+#define FA_MAX_SPLITS 256
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char *fa_status_string(fa_status_t status);
+
+/* Library version, (major << 16) | (minor << 8) | patch. */
+int fa_version(void);
+
+/* Argument checks alone (no HIP call, no device access): returns the status
+ * fa_fwd would return for these arguments before touching the GPU.  Pointers
+ * are compared and tested for alignment only, never dereferenced. */
+fa_status_t fa_validate(const void *q, const void *k, const void *v, const void *o,
+                        const float *lse, int B, int Hq, int Hkv, int Nq, int Nk, int D,
+                        int causal, float scale, fa_dtype_t in_dtype, fa_dtype_t out_dtype);
+
+/* Attention forward with input and output in the same element type. */
+fa_status_t fa_fwd_f16(const void *q, const void *k, const void *v, void *o, float *lse,
+                       int B, int Hq, int Hkv, int Nq, int Nk, int D, int causal,
+                       float scale, void *stream);
+fa_status_t fa_fwd_bf16(const void *q, const void *k, const void *v, void *o, float *lse,
+                        int B, int Hq, int Hkv, int Nq, int Nk, int D, int causal,
+                        float scale, void *stream);
+fa_status_t fa_fwd_f32(const void *q, const void *k, const void *v, void *o, float *lse,
+                       int B, int Hq, int Hkv, int Nq, int Nk, int D, int causal,
+                       float scale, void *stream);
+
+/* Generic form: out_dtype is in_dtype, or FA_F32 to receive the kernel's fp32
+ * result before the final rounding (same kernels, same arithmetic). */
+fa_status_t fa_fwd(const void *q, const void *k, const void *v, void *o, float *lse, int B,
+                   int Hq, int Hkv, int Nq, int Nk, int D, int causal, float scale,
+                   void *stream, fa_dtype_t in_dtype, fa_dtype_t out_dtype);
+
+/* Decode path with an explicit split count (Nq == 1 and fp16 / bf16 with
+ * D in {64, 128} only; otherwise behaves like fa_fwd).  num_splits = 0 picks
+ * the count fa_fwd would use; 1..FA_MAX_SPLITS forces it (splits left
+ * without keys are allowed and contribute nothing to the merge). */
+fa_status_t fa_fwd_splitkv(const void *q, const void *k, const void *v, void *o, float *lse,
+                           int B, int Hq, int Hkv, int Nq, int Nk, int D, int causal,
+                           float scale, void *stream, fa_dtype_t in_dtype,
+                           fa_dtype_t out_dtype, int num_splits);
+
+/* Bytes of decode workspace a call with these sizes needs (0 when the call
+ * takes no split-KV path).  num_splits as in fa_fwd_splitkv. */
+size_t fa_workspace_bytes(int B, int Hq, int Hkv, int Nq, int Nk, int D, fa_dtype_t in_dtype,
+                          int num_splits);
+
+/* Frees the library-owned workspace of the current device (synchronises the
+ * device first).  Safe to call when none is held. */
+fa_status_t fa_release_workspace(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FA_H_ */

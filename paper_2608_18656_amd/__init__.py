@@ -1,0 +1,143 @@
+"""MI355X (gfx950) FlashAttention forward: MHA / GQA / MQA, prefill and decode.
+
+Thin Python layer over the C ABI in include/fa.h (see ``_lib``); PyTorch is
+used only for device memory and the current HIP stream.  Import is cheap: the
+HIP library is loaded on first use and its absence raises (no CPU fallback).
+"""
+from __future__ import annotations
+
+import math
+
+__all__ = ["fwd", "fwd_splitkv", "FaError", "validate", "workspace_bytes", "release_workspace",
+           "version", "DTYPE_CODES"]
+
+
+class FaError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{message} (status {status})")
+        self.status = status
+
+
+def _torch():
+    import torch
+
+    return torch
+
+
+def _codes():
+    torch = _torch()
+    return {torch.float16: 0, torch.bfloat16: 1, torch.float32: 2}
+
+
+DTYPE_CODES = {"f16": 0, "bf16": 1, "f32": 2}
+
+
+def _check(lib, st: int):
+    if st != 0:
+        raise FaError(st, lib.fa_status_string(st).decode())
+
+
+def _prepare(q, k, v, out, lse, out_dtype, return_lse):
+    torch = _torch()
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be a GPU tensor")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous ([B, N, H, D] row-major)")
+        if t.dim() != 4:
+            raise ValueError(f"{name} must be 4-D [B, N, H, D]")
+    if not (q.device == k.device == v.device):
+        raise ValueError("q, k, v must be on the same device")
+    if not (q.dtype == k.dtype == v.dtype) or q.dtype not in _codes():
+        raise ValueError("q, k, v must share one dtype among float16, bfloat16, float32")
+    B, Nq, Hq, D = q.shape
+    Bk, Nk, Hkv, Dk = k.shape
+    if tuple(v.shape) != tuple(k.shape) or Bk != B or Dk != D:
+        raise ValueError("k and v must be [B, Nk, Hkv, D] with q's B and D")
+    odt = q.dtype if out_dtype is None else out_dtype
+    if out is None:
+        out = torch.empty((B, Nq, Hq, D), dtype=odt, device=q.device)
+    elif (tuple(out.shape) != (B, Nq, Hq, D) or out.dtype != odt or not out.is_contiguous()
+          or out.device != q.device):
+        raise ValueError("out must be a contiguous [B, Nq, Hq, D] tensor of the output dtype")
+    if lse is None and return_lse:
+        lse = torch.empty((B, Hq, Nq), dtype=torch.float32, device=q.device)
+    elif lse is not None and (tuple(lse.shape) != (B, Hq, Nq) or lse.dtype != torch.float32
+                              or not lse.is_contiguous() or lse.device != q.device):
+        raise ValueError("lse must be a contiguous float32 [B, Hq, Nq] tensor")
+    return (B, Hq, Hkv, Nq, Nk, D), out, lse, odt
+
+
+def fwd(q, k, v, causal: bool = False, scale: float | None = None, out=None, lse=None,
+        out_dtype=None, return_lse: bool = True, num_splits: int | None = None):
+    """Attention forward o = softmax(scale * q k^T) v on the GPU.
+
+    q [B, Nq, Hq, D], k and v [B, Nk, Hkv, D] (contiguous, same dtype and
+    device); Hq must be a multiple of Hkv (query head h uses key/value head
+    h // (Hq // Hkv)); ``causal`` uses the bottom-right mask (key j visible to
+    query i iff j <= i + Nk - Nq).  ``scale`` defaults to 1/sqrt(D).
+    ``out_dtype=torch.float32`` returns the kernel's fp32 result before the
+    final rounding.  ``num_splits`` forces the decode split count (decode
+    shapes only).  Returns (out, lse) with lse [B, Hq, Nq] float32 natural-log
+    log-sum-exp (None if return_lse is False and no lse tensor was given).
+    """
+    from . import _lib
+
+    lib = _lib.load()
+    torch = _torch()
+    (B, Hq, Hkv, Nq, Nk, D), out, lse, odt = _prepare(q, k, v, out, lse, out_dtype, return_lse)
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    codes = _codes()
+    stream = torch.cuda.current_stream(q.device).cuda_stream
+    args = (q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+            lse.data_ptr() if lse is not None else None, B, Hq, Hkv, Nq, Nk, D,
+            int(bool(causal)), float(scale), stream, codes[q.dtype], codes.get(odt, -1))
+    with torch.cuda.device(q.device):
+        if num_splits is None:
+            st = lib.fa_fwd(*args)
+        else:
+            st = lib.fa_fwd_splitkv(*args, int(num_splits))
+    _check(lib, st)
+    return out, lse
+
+
+def fwd_splitkv(q, k, v, num_splits: int, **kw):
+    """``fwd`` with an explicit decode split count (0 = default choice)."""
+    return fwd(q, k, v, num_splits=num_splits, **kw)
+
+
+def validate(q_ptr, k_ptr, v_ptr, o_ptr, lse_ptr, B, Hq, Hkv, Nq, Nk, D, causal, scale,
+             in_dtype: str, out_dtype: str | None = None) -> int:
+    """Status code of the library's host-side argument checks (no GPU use)."""
+    from . import _lib
+
+    lib = _lib.load()
+    def code(x):
+        return DTYPE_CODES[x] if x in DTYPE_CODES else int(x)
+
+    in_code = code(in_dtype)
+    out_code = in_code if out_dtype is None else code(out_dtype)
+    return int(lib.fa_validate(q_ptr, k_ptr, v_ptr, o_ptr, lse_ptr, B, Hq, Hkv, Nq, Nk, D,
+                               int(causal), float(scale), in_code, out_code))
+
+
+def workspace_bytes(B, Hq, Hkv, Nq, Nk, D, in_dtype: str, num_splits: int = 0) -> int:
+    from . import _lib
+
+    return int(_lib.load().fa_workspace_bytes(B, Hq, Hkv, Nq, Nk, D, DTYPE_CODES[in_dtype],
+                                              num_splits))
+
+
+def release_workspace():
+    from . import _lib
+
+    lib = _lib.load()
+    _check(lib, lib.fa_release_workspace())
+
+
+def version() -> tuple:
+    from . import _lib
+
+    v = _lib.load().fa_version()
+    return (v >> 16, (v >> 8) & 0xFF, v & 0xFF)

@@ -1,0 +1,197 @@
+// fa_api.hip -- the exported C entry points: argument validation, dispatch to
+// the prefill / decode / generic kernels, and the decode workspace.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <mutex>
+
+#include "../../include/fa.h"
+#include "fa_internal.h"
+
+namespace {
+
+size_t esize(fa_dtype_t t) { return t == FA_F32 ? 4 : 2; }
+
+bool overlaps(const void *a, size_t na, const void *b, size_t nb) {
+    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+    return x < y + nb && y < x + na;
+}
+
+bool mul_ok(long long a, long long b, long long *r) {
+    if (a > 0 && b > 0 && a > (long long)(INT64_MAX / 4) / b) return false;
+    *r = a * b;
+    return true;
+}
+
+// Device workspace for the split-KV partial results (one per device).
+struct Workspace {
+    void *ptr = nullptr;
+    size_t bytes = 0;
+};
+constexpr int kMaxDevices = 64;
+Workspace g_ws[kMaxDevices];
+std::mutex g_ws_mu;
+
+fa_status_t get_workspace(size_t need, void **out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return FA_ERR_HIP;
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    Workspace &w = g_ws[dev];
+    if (w.bytes < need) {
+        if (w.ptr) {
+            // earlier calls may still be reading the old buffer
+            if (hipDeviceSynchronize() != hipSuccess) return FA_ERR_HIP;
+            if (hipFree(w.ptr) != hipSuccess) return FA_ERR_HIP;
+            w.ptr = nullptr;
+            w.bytes = 0;
+        }
+        size_t sz = need < ((size_t)1 << 20) ? ((size_t)1 << 20) : need;
+        if (hipMalloc(&w.ptr, sz) != hipSuccess) {
+            w.ptr = nullptr;
+            (void)hipGetLastError();
+            return FA_ERR_WORKSPACE;
+        }
+        w.bytes = sz;
+    }
+    *out = w.ptr;
+    return FA_OK;
+}
+
+fa_status_t run(const void *q, const void *k, const void *v, void *o, float *lse, int B, int Hq,
+                int Hkv, int Nq, int Nk, int D, int causal, float scale, void *stream,
+                fa_dtype_t in, fa_dtype_t out, int splits_req) {
+    fa_status_t st = fa_validate(q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, in, out);
+    if (st != FA_OK) return st;
+    if (splits_req < 0 || splits_req > FA_MAX_SPLITS) return FA_ERR_SPLITS;
+    fa::Problem p{q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, in, out};
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    hipError_t e;
+    if (fa::decode_supported(Nq, D, in)) {
+        const int S = splits_req > 0 ? splits_req : fa::decode_default_splits(B, Hq, Hkv, Nk, D);
+        void *ws = nullptr;
+        st = get_workspace(fa::decode_workspace_bytes(B, Hq, D, S), &ws);
+        if (st != FA_OK) return st;
+        e = fa::launch_decode(p, S, ws, s);
+    } else if (fa::prefill_supported(D, in)) {
+        e = fa::launch_prefill(p, s);
+    } else {
+        e = fa::launch_generic(p, s);
+    }
+    return e == hipSuccess ? FA_OK : FA_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *fa_status_string(fa_status_t s) {
+    switch (s) {
+    case FA_OK: return "FA_OK";
+    case FA_ERR_NULL: return "FA_ERR_NULL: q, k, v or o is NULL";
+    case FA_ERR_DIM: return "FA_ERR_DIM: a size is < 1 or the tensors are too large";
+    case FA_ERR_GQA_RATIO: return "FA_ERR_GQA_RATIO: Hq is not a multiple of Hkv";
+    case FA_ERR_HEAD_DIM: return "FA_ERR_HEAD_DIM: D must be a multiple of 8 and at most 256";
+    case FA_ERR_CAUSAL_SHAPE: return "FA_ERR_CAUSAL_SHAPE: causal requires Nq <= Nk";
+    case FA_ERR_SCALE: return "FA_ERR_SCALE: scale is NaN or infinite";
+    case FA_ERR_ALIGN: return "FA_ERR_ALIGN: a tensor pointer is misaligned";
+    case FA_ERR_ALIAS: return "FA_ERR_ALIAS: o or lse overlaps another tensor";
+    case FA_ERR_DTYPE: return "FA_ERR_DTYPE: unsupported dtype combination";
+    case FA_ERR_WORKSPACE: return "FA_ERR_WORKSPACE: workspace allocation failed";
+    case FA_ERR_HIP: return "FA_ERR_HIP: HIP runtime or launch error";
+    case FA_ERR_SPLITS: return "FA_ERR_SPLITS: num_splits out of range";
+    }
+    return "unknown fa_status_t";
+}
+
+int fa_version(void) { return (0 << 16) | (1 << 8) | 0; }
+
+fa_status_t fa_validate(const void *q, const void *k, const void *v, const void *o,
+                        const float *lse, int B, int Hq, int Hkv, int Nq, int Nk, int D,
+                        int causal, float scale, fa_dtype_t in, fa_dtype_t out) {
+    if (!q || !k || !v || !o) return FA_ERR_NULL;
+    if (B < 1 || Hq < 1 || Hkv < 1 || Nq < 1 || Nk < 1 || D < 1) return FA_ERR_DIM;
+    if (in != FA_F16 && in != FA_BF16 && in != FA_F32) return FA_ERR_DTYPE;
+    if (out != in && out != FA_F32) return FA_ERR_DTYPE;
+    if (Hq % Hkv != 0) return FA_ERR_GQA_RATIO;
+    if (D % 8 != 0 || D > 256) return FA_ERR_HEAD_DIM;
+    if (causal && Nq > Nk) return FA_ERR_CAUSAL_SHAPE;
+    if (!std::isfinite(scale)) return FA_ERR_SCALE;
+    long long nq, nk, t;
+    if (!mul_ok((long long)B * Nq, (long long)Hq * D, &nq) ||
+        !mul_ok((long long)B * Nk, (long long)Hkv * D, &nk) ||
+        !mul_ok((long long)B * Hq, (long long)Nq, &t))
+        return FA_ERR_DIM;
+    const uintptr_t a16 = 15;
+    if ((reinterpret_cast<uintptr_t>(q) & a16) || (reinterpret_cast<uintptr_t>(k) & a16) ||
+        (reinterpret_cast<uintptr_t>(v) & a16) || (reinterpret_cast<uintptr_t>(o) & a16) ||
+        (reinterpret_cast<uintptr_t>(lse) & 3))
+        return FA_ERR_ALIGN;
+    const size_t qb = (size_t)nq * esize(in), kb = (size_t)nk * esize(in);
+    const size_t ob = (size_t)nq * esize(out), lb = (size_t)t * sizeof(float);
+    if (overlaps(o, ob, q, qb) || overlaps(o, ob, k, kb) || overlaps(o, ob, v, kb))
+        return FA_ERR_ALIAS;
+    if (lse && (overlaps(lse, lb, q, qb) || overlaps(lse, lb, k, kb) ||
+                overlaps(lse, lb, v, kb) || overlaps(lse, lb, o, ob)))
+        return FA_ERR_ALIAS;
+    return FA_OK;
+}
+
+fa_status_t fa_fwd(const void *q, const void *k, const void *v, void *o, float *lse, int B,
+                   int Hq, int Hkv, int Nq, int Nk, int D, int causal, float scale, void *stream,
+                   fa_dtype_t in_dtype, fa_dtype_t out_dtype) {
+    return run(q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, stream, in_dtype, out_dtype,
+               0);
+}
+
+fa_status_t fa_fwd_f16(const void *q, const void *k, const void *v, void *o, float *lse, int B,
+                       int Hq, int Hkv, int Nq, int Nk, int D, int causal, float scale,
+                       void *stream) {
+    return run(q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, stream, FA_F16, FA_F16, 0);
+}
+
+fa_status_t fa_fwd_bf16(const void *q, const void *k, const void *v, void *o, float *lse, int B,
+                        int Hq, int Hkv, int Nq, int Nk, int D, int causal, float scale,
+                        void *stream) {
+    return run(q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, stream, FA_BF16, FA_BF16,
+               0);
+}
+
+fa_status_t fa_fwd_f32(const void *q, const void *k, const void *v, void *o, float *lse, int B,
+                       int Hq, int Hkv, int Nq, int Nk, int D, int causal, float scale,
+                       void *stream) {
+    return run(q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, stream, FA_F32, FA_F32, 0);
+}
+
+fa_status_t fa_fwd_splitkv(const void *q, const void *k, const void *v, void *o, float *lse,
+                           int B, int Hq, int Hkv, int Nq, int Nk, int D, int causal, float scale,
+                           void *stream, fa_dtype_t in_dtype, fa_dtype_t out_dtype,
+                           int num_splits) {
+    return run(q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, stream, in_dtype, out_dtype,
+               num_splits);
+}
+
+size_t fa_workspace_bytes(int B, int Hq, int Hkv, int Nq, int Nk, int D, fa_dtype_t in_dtype,
+                          int num_splits) {
+    if (B < 1 || Hq < 1 || Hkv < 1 || Nk < 1 || Hq % Hkv != 0) return 0;
+    if (!fa::decode_supported(Nq, D, in_dtype)) return 0;
+    if (num_splits < 0 || num_splits > FA_MAX_SPLITS) return 0;
+    const int S = num_splits > 0 ? num_splits : fa::decode_default_splits(B, Hq, Hkv, Nk, D);
+    return fa::decode_workspace_bytes(B, Hq, D, S);
+}
+
+fa_status_t fa_release_workspace(void) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return FA_ERR_HIP;
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    Workspace &w = g_ws[dev];
+    if (w.ptr) {
+        if (hipDeviceSynchronize() != hipSuccess) return FA_ERR_HIP;
+        if (hipFree(w.ptr) != hipSuccess) return FA_ERR_HIP;
+    }
+    w.ptr = nullptr;
+    w.bytes = 0;
+    return FA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,175 @@
+// fa_generic.hip -- vector-ALU attention forward for the cases the matrix-core
+// kernels do not take: fp32 inputs, and fp16 / bf16 with a head dimension
+// other than 64 or 128 (any D with D % 8 == 0 and D <= 256).
+//
+// All arithmetic is fp32.  A workgroup of 256 threads owns 64 query rows of
+// one query head; four consecutive threads share a row and each holds an
+// interleaved quarter of its D columns (pairs d = 8 i + 2 t + {0, 1}).  Keys
+// are streamed in LDS tiles; per tile the scores of all tile keys are formed
+// (partial dot products reduced over the four threads of the row), then the
+// running maximum / sum / accumulator are updated once for the tile -- the
+// blocked form (Alg. 2) of the streaming recurrence of Alg. 1 -- and the
+// accumulator is normalised after the last visible tile.
+#include "fa_common.h"
+#include "fa_internal.h"
+
+namespace fa {
+namespace {
+
+struct GenericArgs {
+    const void *q, *k, *v;
+    void *o;
+    float *lse;
+    int B, Hq, Hkv, Nq, Nk, D;
+    float c;   // scale * log2(e), signed
+    int nmb;   // row blocks of 64
+};
+
+template <typename T> struct Scalar { typedef T type; };
+template <> struct Scalar<f16_t> { typedef _Float16 type; };
+template <> struct Scalar<bf16_t> { typedef __bf16 type; };
+
+template <typename TIN, typename TOUT, int DMAX, bool CAUSAL>
+__global__ __launch_bounds__(256) void generic_kernel(GenericArgs a) {
+    typedef typename Scalar<TIN>::type S;
+    constexpr int KT = 16;                       // keys per LDS tile
+    constexpr int NP = DMAX / 8;                 // column pairs per thread
+    __shared__ float ks[KT * DMAX];
+    __shared__ float vs[KT * DMAX];
+
+    const int tid = threadIdx.x, row = tid >> 2, part = tid & 3;
+    int bid = blockIdx.x;
+    const int mb = a.nmb - 1 - bid % a.nmb;
+    bid /= a.nmb;
+    const int h = bid % a.Hq;
+    const int b = bid / a.Hq;
+    const int G = a.Hq / a.Hkv, g = h / G;
+    const int D = a.D, Nq = a.Nq, Nk = a.Nk;
+    const int qi = mb * 64 + row;
+    const int off = Nk - Nq;
+    const int last_blk = min(mb * 64 + 64, Nq) - 1;
+    const int kend = CAUSAL ? min(Nk, last_blk + off + 1) : Nk;
+    const int myend = CAUSAL ? min(Nk, qi + off + 1) : Nk;
+
+    float q0[NP], q1[NP], o0[NP], o1[NP];
+    const S *qp = reinterpret_cast<const S *>(a.q) + ((size_t)((size_t)b * Nq + qi) * a.Hq + h) * D;
+#pragma unroll
+    for (int i = 0; i < NP; ++i) {
+        const int d = 8 * i + 2 * part;
+        q0[i] = (qi < Nq && d < D) ? to_f32(qp[d]) : 0.f;
+        q1[i] = (qi < Nq && d < D) ? to_f32(qp[d + 1]) : 0.f;
+        o0[i] = 0.f;
+        o1[i] = 0.f;
+    }
+    float m = -INFINITY, lsum = 0.f;
+    const S *kb_ = reinterpret_cast<const S *>(a.k);
+    const S *vb_ = reinterpret_cast<const S *>(a.v);
+
+    for (int kb = 0; kb < kend; kb += KT) {
+        __syncthreads();
+        // columns d >= D are zero-filled so the inner loops need no guard
+        for (int e = tid; e < KT * DMAX; e += 256) {
+            const int kk = e / DMAX, d = e % DMAX, key = kb + kk;
+            float kv = 0.f, vv = 0.f;
+            if (key < Nk && d < D) {
+                const size_t o = ((size_t)((size_t)b * Nk + key) * a.Hkv + g) * D + d;
+                kv = to_f32(kb_[o]);
+                vv = to_f32(vb_[o]);
+            }
+            ks[kk * DMAX + d] = kv;
+            vs[kk * DMAX + d] = vv;
+        }
+        __syncthreads();
+        float x[KT];
+        float tmax = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < KT; ++j) {
+            float acc = 0.f;
+#pragma unroll
+            for (int i = 0; i < NP; ++i) {
+                const int d = 8 * i + 2 * part;
+                acc += q0[i] * ks[j * DMAX + d] + q1[i] * ks[j * DMAX + d + 1];
+            }
+            acc += __shfl_xor(acc, 1);
+            acc += __shfl_xor(acc, 2);
+            const bool vis = kb + j < myend;
+            x[j] = vis ? acc * a.c : -INFINITY;
+            tmax = __builtin_fmaxf(tmax, x[j]);
+        }
+        const float m_new = __builtin_fmaxf(m, tmax);
+        if (m_new == -INFINITY) continue;   // nothing visible yet for this row
+        const float alpha = (m == -INFINITY) ? 0.f : exp2_fast(m - m_new);
+        m = m_new;
+        lsum *= alpha;
+#pragma unroll
+        for (int i = 0; i < NP; ++i) {
+            o0[i] *= alpha;
+            o1[i] *= alpha;
+        }
+#pragma unroll
+        for (int j = 0; j < KT; ++j) {
+            const float p = (x[j] == -INFINITY) ? 0.f : exp2_fast(x[j] - m);
+            lsum += p;
+#pragma unroll
+            for (int i = 0; i < NP; ++i) {
+                const int d = 8 * i + 2 * part;
+                o0[i] += p * vs[j * DMAX + d];
+                o1[i] += p * vs[j * DMAX + d + 1];
+            }
+        }
+    }
+    if (qi >= Nq) return;
+    const float inv = 1.f / lsum;
+    TOUT *op = reinterpret_cast<TOUT *>(a.o) + ((size_t)((size_t)b * Nq + qi) * a.Hq + h) * D;
+#pragma unroll
+    for (int i = 0; i < NP; ++i) {
+        const int d = 8 * i + 2 * part;
+        if (d < D) {
+            op[d] = from_f32<TOUT>(o0[i] * inv);
+            op[d + 1] = from_f32<TOUT>(o1[i] * inv);
+        }
+    }
+    if (a.lse && part == 0) a.lse[((size_t)b * a.Hq + h) * Nq + qi] = (m + log2f(lsum)) * kLn2;
+}
+
+template <typename TIN, typename TOUT, int DMAX>
+hipError_t launch_t(const Problem &p, hipStream_t stream) {
+    GenericArgs a;
+    a.q = p.q; a.k = p.k; a.v = p.v; a.o = p.o; a.lse = p.lse;
+    a.B = p.B; a.Hq = p.Hq; a.Hkv = p.Hkv; a.Nq = p.Nq; a.Nk = p.Nk; a.D = p.D;
+    a.c = p.scale * kLog2e;
+    a.nmb = (p.Nq + 63) / 64;
+    const long long nblocks = (long long)a.nmb * p.B * p.Hq;
+    if (nblocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+    if (p.causal)
+        hipLaunchKernelGGL((generic_kernel<TIN, TOUT, DMAX, true>), dim3((unsigned)nblocks),
+                           dim3(256), 0, stream, a);
+    else
+        hipLaunchKernelGGL((generic_kernel<TIN, TOUT, DMAX, false>), dim3((unsigned)nblocks),
+                           dim3(256), 0, stream, a);
+    return hipGetLastError();
+}
+
+template <typename TIN, typename TOUT>
+hipError_t launch_d(const Problem &p, hipStream_t s) {
+    if (p.D <= 64) return launch_t<TIN, TOUT, 64>(p, s);
+    if (p.D <= 128) return launch_t<TIN, TOUT, 128>(p, s);
+    return launch_t<TIN, TOUT, 256>(p, s);
+}
+
+}  // namespace
+
+hipError_t launch_generic(const Problem &p, hipStream_t stream) {
+    switch (p.in) {
+    case FA_F32:
+        return launch_d<float, float>(p, stream);
+    case FA_F16:
+        return p.out == FA_F32 ? launch_d<f16_t, float>(p, stream)
+                               : launch_d<f16_t, _Float16>(p, stream);
+    default:
+        return p.out == FA_F32 ? launch_d<bf16_t, float>(p, stream)
+                               : launch_d<bf16_t, __bf16>(p, stream);
+    }
+}
+
+}  // namespace fa

@@ -1,0 +1,34 @@
+// fa_internal.h -- host-side launcher declarations shared by the library's
+// translation units (not part of the public interface in include/fa.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+
+#include "../../include/fa.h"
+
+namespace fa {
+
+struct Problem {
+    const void *q, *k, *v;
+    void *o;
+    float *lse;
+    int B, Hq, Hkv, Nq, Nk, D;
+    int causal;
+    float scale;
+    fa_dtype_t in, out;
+};
+
+// Each launcher enqueues its kernels on `stream` and returns the first HIP
+// error (hipSuccess when the launch was accepted).
+hipError_t launch_prefill(const Problem &p, hipStream_t stream);
+hipError_t launch_generic(const Problem &p, hipStream_t stream);
+hipError_t launch_decode(const Problem &p, int splits, void *workspace, hipStream_t stream);
+
+// Decode split planning (shared by the dispatcher and fa_workspace_bytes).
+bool decode_supported(int Nq, int D, fa_dtype_t in);
+bool prefill_supported(int D, fa_dtype_t in);
+int decode_default_splits(int B, int Hq, int Hkv, int Nk, int D);
+size_t decode_workspace_bytes(int B, int Hq, int D, int splits);
+
+}  // namespace fa

@@ -1,0 +1,98 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports
+every function include/fa.h declares, and its argument validation returns
+the documented status codes before touching the device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_18656_amd import _lib, validate, workspace_bytes
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fa.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fa_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_library_loads_and_exports_every_declared_symbol():
+    lib = _lib.load()
+    names = declared_functions()
+    assert len(names) >= 10
+    assert set(names) == set(_lib.EXPORTS)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert lib.fa_version() == (0 << 16) | (1 << 8)
+
+
+def test_status_strings():
+    lib = _lib.load()
+    for code, name in _lib.STATUS_NAMES.items():
+        assert lib.fa_status_string(code).decode().startswith(name)
+
+
+A = 1 << 20   # fake, 16-byte aligned, non-overlapping "device" addresses
+GOOD = dict(q=A, k=9 * A, v=17 * A, o=25 * A, lse=33 * A)
+DIMS = dict(B=1, Hq=4, Hkv=2, Nq=8, Nk=8, D=64, causal=1, scale=0.125)
+
+
+def call(dt="f16", out=None, **over):
+    p = dict(GOOD)
+    p.update(DIMS)
+    p.update(over)
+    return validate(p["q"], p["k"], p["v"], p["o"], p["lse"], p["B"], p["Hq"], p["Hkv"], p["Nq"],
+                    p["Nk"], p["D"], p["causal"], p["scale"], dt, out)
+
+
+@pytest.mark.parametrize("over,code", [
+    ({}, 0),
+    ({"q": None}, 1), ({"k": None}, 1), ({"v": None}, 1), ({"o": None}, 1),
+    ({"B": 0}, 2), ({"Hq": 0}, 2), ({"Nq": 0}, 2), ({"Nk": -1}, 2), ({"D": 0}, 2),
+    ({"Hq": 6, "Hkv": 4}, 3),
+    ({"D": 60}, 4), ({"D": 264}, 4),
+    ({"Nq": 9, "Nk": 8}, 5),
+    ({"scale": float("nan")}, 6), ({"scale": float("inf")}, 6),
+    ({"q": A + 8}, 7), ({"o": 25 * A + 2}, 7), ({"lse": 33 * A + 2}, 7),
+    ({"o": A + 64}, 8), ({"lse": 9 * A + 16}, 8), ({"lse": 25 * A}, 8),
+])
+def test_validation_status_codes(over, code):
+    assert call(**over) == code
+
+
+def test_validation_accepts_edge_shapes_and_scales():
+    assert call(lse=None) == 0                      # lse optional
+    assert call(causal=0, Nq=9, Nk=8) == 0          # non-causal Nq > Nk is fine
+    assert call(scale=0.0) == 0 and call(scale=-2.0) == 0
+    assert call(D=8) == 0 and call(D=256) == 0
+    assert call(Hkv=1) == 0 and call(Hkv=4) == 0   # MQA and MHA
+
+
+def test_validation_dtype_rules():
+    assert call("bf16") == 0 and call("f32") == 0
+    assert call("f16", "f32") == 0 and call("bf16", "f32") == 0   # fp32 verify output
+    assert call("f16", "bf16") == 9 and call("f32", "f16") == 9
+    assert call(7) == 9
+
+
+def test_validation_rejects_size_overflow():
+    assert call(B=1 << 30, Nq=1 << 30, Nk=1 << 30, causal=0) == 2
+
+
+def test_workspace_bytes():
+    # decode: B * Hq * S * (D + 2) floats; other shapes need none
+    assert workspace_bytes(16, 32, 8, 1, 8192, 128, "bf16", 8) == 16 * 32 * 8 * 130 * 4
+    assert workspace_bytes(16, 32, 8, 1, 8192, 128, "bf16", 0) > 0
+    assert workspace_bytes(1, 32, 8, 2048, 2048, 64, "bf16") == 0
+    assert workspace_bytes(1, 2, 2, 1, 128, 64, "f32") == 0
+    assert workspace_bytes(1, 2, 2, 1, 128, 64, "f16", 300) == 0
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    monkeypatch.setattr(_lib, "LIB_PATH", str(tmp_path / "absent.so"))
+    monkeypatch.setattr(_lib, "_lib", None)
+    with pytest.raises(FileNotFoundError):
+        _lib.load()
