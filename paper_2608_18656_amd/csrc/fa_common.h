@@ -96,11 +96,19 @@ __device__ __forceinline__ half8_t pack_f16x8(float a0, float a1, float a2, floa
     return h;
 }
 
-// Exchange with the lane 32 positions away (lanes l and l^32).
-__device__ __forceinline__ float swap_half(float x) {
+// Reductions over the lane pair (l, l^32).  v_permlane32_swap exchanges the
+// upper half of its first operand with the lower half of its second; with the
+// same value in both, the two results of every lane are the pair's two values
+// (one from each half), whichever result holds which.
+__device__ __forceinline__ float pair_max(float x) {
     auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
                                               false);
-    return __uint_as_float(r[0]);
+    return __builtin_fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                              false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
 __device__ __forceinline__ float max3(float a, float b, float c) {

@@ -197,7 +197,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
             for (int r = 0; r < 8; ++r) mx = max3(mx, s0[2 * r], s0[2 * r + 1]);
 #pragma unroll
             for (int r = 0; r < 8; ++r) mx = max3(mx, s1[2 * r], s1[2 * r + 1]);
-            mx = __builtin_fmaxf(mx, swap_half(mx));
+            mx = pair_max(mx);
             const float m_tile = (mx == -INFINITY) ? -INFINITY : mx * a.c;
             // ---- lazy rescale of accumulator and sum
             const float m_new = __builtin_fmaxf(m_run, m_tile);
@@ -248,7 +248,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
 
     if (!wave_live) return;
     // ---- final normalisation and stores
-    const float l_tot = l_run + swap_half(l_run);
+    const float l_tot = pair_sum(l_run);
     const float inv = 1.f / l_tot;
     if (qi < Nq) {
         typedef TOUT OT;
