@@ -75,16 +75,22 @@ template <typename V> __device__ __forceinline__ uint4_t as_u4(V v) {
 
 // bf16 x8 (as raw 16-byte word) -> f16 x8 (raw), round to nearest even.
 __device__ __forceinline__ uint4_t bf16x8_to_f16x8(uint4_t u) {
-    uint4_t r;
+    half8_t h;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        float lo = __uint_as_float(u[i] << 16);
-        float hi = __uint_as_float(u[i] & 0xffff0000u);
-        _Float16 a = (_Float16)lo, b = (_Float16)hi;
-        r[i] = (uint32_t)__builtin_bit_cast(unsigned short, a) |
-               ((uint32_t)__builtin_bit_cast(unsigned short, b) << 16);
+        h[2 * i] = (_Float16)__uint_as_float(u[i] << 16);
+        h[2 * i + 1] = (_Float16)__uint_as_float(u[i] & 0xffff0000u);
     }
-    return r;
+    return __builtin_bit_cast(uint4_t, h);
+}
+
+// Two fp32 values -> packed f16 pair (first in the low half), round to nearest even.
+__device__ __forceinline__ unsigned pack_f16x2(float lo, float hi) {
+    typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+    half2_t h;
+    h[0] = (_Float16)lo;
+    h[1] = (_Float16)hi;
+    return __builtin_bit_cast(unsigned, h);
 }
 
 // Pack 8 fp32 values to f16 x8, round to nearest even.
@@ -132,5 +138,9 @@ __device__ __forceinline__ uint4_t ld16(const void *p) {
     return *reinterpret_cast<const uint4_t *>(p);
 }
 __device__ __forceinline__ void st16(void *p, uint4_t v) { *reinterpret_cast<uint4_t *>(p) = v; }
+// Streaming 16-byte load for data read exactly once (non-temporal hint).
+__device__ __forceinline__ uint4_t ld16_stream(const void *p) {
+    return __builtin_nontemporal_load(reinterpret_cast<const uint4_t *>(p));
+}
 
 }  // namespace fa

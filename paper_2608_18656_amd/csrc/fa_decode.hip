@@ -123,7 +123,8 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
 #pragma unroll
             for (int ks = 0; ks < KST; ++ks) {
                 kn[hf][ks] = uint4_t{0u, 0u, 0u, 0u};
-                if (key < k1) kn[hf][ks] = ld16(kbase + head_off + key * row_stride + 32 * ks + 8 * lg);
+                if (key < k1)
+                    kn[hf][ks] = ld16_stream(kbase + head_off + key * row_stride + 32 * ks + 8 * lg);
             }
         }
 #pragma unroll
@@ -131,7 +132,7 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
             const int c = l + 64 * i;
             const int key = kb + c / CPR, cc = c % CPR;
             vr[i] = uint4_t{0u, 0u, 0u, 0u};
-            if (key < k1) vr[i] = ld16(vbase + head_off + key * row_stride + 8 * cc);
+            if (key < k1) vr[i] = ld16_stream(vbase + head_off + key * row_stride + 8 * cc);
         }
     };
     auto vstore = [&]() {
@@ -265,26 +266,53 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
 
 // Merge of the S partial results of one (batch, query head): lse-weighted sum
 // of the unnormalised accumulators, final normalisation, log-sum-exp output.
+// All loads of one phase are independent, so each phase costs one memory
+// round trip: (1) every split's max and sum, (2) the accumulator columns.
 template <typename TOUT, int D>
 __global__ __launch_bounds__(D) void decode_combine_kernel(const float *__restrict__ opart,
                                                           const float *__restrict__ mpart,
                                                           const float *__restrict__ lpart,
                                                           void *o, float *lse, int S) {
-    const int bh = blockIdx.x, d = threadIdx.x;
+    __shared__ float wgt[FA_MAX_SPLITS];
+    __shared__ float lsp[FA_MAX_SPLITS];
+    __shared__ float red[2 * (D / 64)];
+    const int bh = blockIdx.x, t = threadIdx.x, lane = t & 63, wv = t >> 6;
     const float *mp = mpart + (size_t)bh * S;
     const float *lp = lpart + (size_t)bh * S;
     const float *op = opart + (size_t)bh * S * D;
-    float M = -INFINITY;
-    for (int s = 0; s < S; ++s) M = __builtin_fmaxf(M, mp[s]);
-    float L = 0.f, acc = 0.f;
-    for (int s = 0; s < S; ++s) {
-        const float ms = mp[s];
-        const float wgt = (ms == -INFINITY) ? 0.f : exp2_fast(ms - M);
-        L += wgt * lp[s];
-        acc += wgt * op[(size_t)s * D + d];
+    float mloc = -INFINITY;
+    for (int s = t; s < S; s += D) {
+        const float m = mp[s];
+        wgt[s] = m;
+        lsp[s] = lp[s];
+        mloc = __builtin_fmaxf(mloc, m);
     }
-    reinterpret_cast<TOUT *>(o)[(size_t)bh * D + d] = from_f32<TOUT>(acc / L);
-    if (lse && d == 0) lse[bh] = (M + log2f(L)) * kLn2;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) mloc = __builtin_fmaxf(mloc, __shfl_xor(mloc, off));
+    if (lane == 0) red[wv] = mloc;
+    __syncthreads();
+    float M = red[0];
+#pragma unroll
+    for (int i = 1; i < D / 64; ++i) M = __builtin_fmaxf(M, red[i]);
+    float lsum = 0.f;
+    for (int s = t; s < S; s += D) {
+        const float m = wgt[s];
+        const float w = (m == -INFINITY) ? 0.f : exp2_fast(m - M);
+        wgt[s] = w;
+        lsum += w * lsp[s];
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) lsum += __shfl_xor(lsum, off);
+    if (lane == 0) red[D / 64 + wv] = lsum;
+    __syncthreads();
+    float L = 0.f;
+#pragma unroll
+    for (int i = 0; i < D / 64; ++i) L += red[D / 64 + i];
+    float acc = 0.f;
+#pragma unroll 8
+    for (int s = 0; s < S; ++s) acc += wgt[s] * op[(size_t)s * D + t];
+    reinterpret_cast<TOUT *>(o)[(size_t)bh * D + t] = from_f32<TOUT>(acc / L);
+    if (lse && t == 0) lse[bh] = (M + log2f(L)) * kLn2;
 }
 
 template <typename TIN, typename TOUT, int D>

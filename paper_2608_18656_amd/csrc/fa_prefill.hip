@@ -1,80 +1,96 @@
 // fa_prefill.hip -- prefill attention forward on gfx950 matrix cores.
 //
-// One workgroup = 4 waves.  Each wave owns 32 query rows of one query head
-// and walks the key sequence in tiles of 64 keys, carrying the running row
-// maximum, running row sum and the unnormalised output accumulator from tile
-// to tile (the blocked streaming softmax of Alg. 2, built on the per-key
-// recurrence of Alg. 1), and normalises once after its last visible tile.
+// Work split.  A workgroup has 8 waves and owns four (query head, 32-row
+// block) slots that read the same key/value head.  When the group size
+// G = Hq/Hkv allows, the four slots are four query heads of one key/value
+// group at the same rows -- the GPU form of the inter-head packing of
+// Sec. 4.1.1 and the GQA reuse of Sec. 4.1.2 (iv): every K/V tile staged in
+// LDS serves four heads, and all slots share one causal extent.  Otherwise
+// (G = 1 or odd) the slots are consecutive row blocks of one head.  Each slot
+// has two waves; keys are streamed in tiles of 64 and wave kh of a slot takes
+// keys 32 kh .. 32 kh + 31 of every tile, so the sequential chain per wave is
+// half the tile work.  The two waves' states are merged through LDS at the end.
 //
-// Head packing (the GPU form of the inter-head packing of Sec. 4.1.1 and the
-// GQA reuse of Sec. 4.1.2 (iv)): when the group size G = Hq/Hkv allows, the
-// four waves of a workgroup take four query heads of the same key/value group
-// at the same query rows, so each K/V tile staged in LDS serves four heads and
-// all four waves have the same causal extent.  Otherwise (G = 1 or odd) the
-// waves take consecutive row blocks of one head.
-//
-// Per tile and wave:
-//   S^T = K_tile Q^T        32x32x16 MFMA, A = K rows from LDS, B = Q rows
-//                           kept in registers for the whole kernel
-//   softmax update          scores stay in the MFMA result registers: lane l
-//                           owns query row l%32, so the row max needs one
-//                           exchange with lane l^32; exp2 with the scale and
-//                           log2(e) folded into one multiply-add
-//   O^T += V_tile^T P^T     32x32x16 fp16 MFMA; P comes straight from the
-//                           score registers (no cross-lane move); V^T operands
-//                           come from LDS with transpose reads
-// The running maximum used as the exponent base is only raised when a row's
-// maximum grows by more than 2^8 (log2 domain), so the accumulator rescale is
-// skipped on most tiles; the result is unchanged because the sum and the
-// accumulator always share the same base.
+// Per wave and tile, the blocked streaming softmax (Alg. 2 state carry over
+// the per-key recurrence of Alg. 1):
+//   S^T = K Q^T        32x32x16 MFMA; A = 32 K rows from LDS, B = the wave's
+//                      32 query rows, kept in registers for the whole kernel
+//   row max / exp2     scores stay in the MFMA result registers; lane l owns
+//                      query row l%32, so the row max needs one exchange with
+//                      lane l^32; scale and log2(e) fold into one multiply-add
+//   O^T += V^T P^T     32x32x16 fp16 MFMA; P straight from the score registers,
+//                      V^T operands read from a transposed copy of the V tile
+//                      that the staging step writes into LDS (a transposing
+//                      LDS read runs at about a third of the plain 16-byte
+//                      read rate on gfx950, so the transpose is paid once per
+//                      tile in the copy instead of once per wave)
+// The exponent base is raised only when a row's maximum grows by more than
+// 2^8 (log2 domain), so the accumulator rescale is skipped on most tiles; sum
+// and accumulator always share the base, so the result is unchanged.
+// Masked scores are -inf and give exactly 0 (the exponent factor is kept
+// strictly positive, also for scale = 0).  Keys past the end are read from a
+// clamped row and masked.  Normalisation happens once, after the last tile.
+#include <type_traits>
+
 #include "fa_common.h"
 #include "fa_internal.h"
 
 namespace fa {
 namespace {
 
-constexpr int BC = 64;        // keys per tile
-constexpr int WR = 32;        // query rows per wave
-constexpr int NW = 4;         // waves per workgroup
+constexpr int BC = 64;        // keys per tile (two halves of 32, one per wave)
+constexpr int WR = 32;        // query rows per slot
+constexpr int NSLOT = 4;      // slots per workgroup
+constexpr int NT = 128 * NSLOT;   // threads per workgroup (two waves per slot)
 constexpr float TAU = 8.0f;   // lazy-rescale threshold (log2 units)
+constexpr int NSTAGE = 3;     // LDS tile stages
 
 struct PrefillArgs {
     const void *q, *k, *v;
     void *o;
     float *lse;
     int B, Hq, Hkv, Nq, Nk;
-    float c;      // |scale| * log2(e)
-    float scale_zero;  // 1 when scale == 0 (all visible weights equal)
-    unsigned qsign;    // 0x80008000 to negate q (scale < 0), else 0
-    int HW;       // query heads per workgroup (1, 2 or 4)
-    int nmb;      // row blocks of 32 * (4 / HW) rows
-    int nhg;      // head groups per key/value head (G / HW)
+    float c;          // max(|scale|, tiny) * log2(e), > 0
+    unsigned qsign;   // 0x80008000 to negate q (scale < 0), else 0
+    int HW;           // query heads per workgroup (1, 2 or 4)
+    int nmb;          // row blocks of 32 * (4 / HW) rows
+    int nhg;          // head groups per key/value head (G / HW)
 };
 
 template <int D> struct Smem {
-    static constexpr int KS = D + 8;    // K row stride in 16-bit elements
-    static constexpr int VS = D + 16;   // V row stride in 16-bit elements
+    static constexpr int KS = D + 8;     // K row stride in 16-bit elements
+    static constexpr int VTS = BC + 8;   // V^T row stride: 64 key positions + pad
     static constexpr int KSZ = BC * KS;
-    static constexpr int VSZ = BC * VS;
+    static constexpr int VSZ = D * VTS;
     static constexpr int STAGE = KSZ + VSZ;
+    static constexpr int MERGE = NSLOT * ((D / 32) * 16 + 2) * 64;   // floats
+    static constexpr int WORDS = (NSTAGE * STAGE) > (2 * MERGE) ? NSTAGE * STAGE : 2 * MERGE;
 };
 
+// The first half of the workgroup stages K, the second half V.
+__device__ __forceinline__ bool kgroup_of(int tid) { return tid < NT / 2; }
+
 template <typename TIN, typename TOUT, int D, bool CAUSAL>
-__global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
+__global__ __launch_bounds__(NT, 1) void prefill_kernel(PrefillArgs a) {
     using S = typename TIN::scalar;
     using V8 = typename TIN::vec8;
     using SM = Smem<D>;
     constexpr int KSTEPS = D / 16;          // QK^T contraction steps
     constexpr int DT = D / 32;              // output column tiles
-    constexpr int LOADS = D / 32;           // 16-byte chunks per thread per K (or V) tile
+    constexpr int LOADS = BC * D / 8 / NT;  // 16-byte chunks per thread per K (or V) tile
     constexpr int CPR = D / 8;              // 16-byte chunks per row
     constexpr bool IN_BF16 = __is_same(TIN, bf16_t);
+    // Issue the next tile's scores during this tile's softmax (D = 64, where
+    // the vector ALU work is as large as the matrix work); at D = 128 the
+    // registers are needed for the larger accumulator instead.
+    constexpr bool PIPE = D == 64;
 
-    __shared__ __attribute__((aligned(16))) unsigned short smem[2 * SM::STAGE];
+    __shared__ __attribute__((aligned(16))) unsigned short smem[SM::WORDS];
 
     const int tid = threadIdx.x;
     const int w = tid >> 6, l = tid & 63, lq = l & 31, lh = l >> 5;
-    const int RB = NW / a.HW;
+    const int kh = w / NSLOT, slot = w % NSLOT;
+    const int RB = NSLOT / a.HW;
     const int per_mb = a.B * a.Hkv * a.nhg;
     const int bid = blockIdx.x;
     const int mb = a.nmb - 1 - bid / per_mb;    // latest rows (most keys) first
@@ -84,7 +100,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     const int g = rest % a.Hkv;
     const int b = rest / a.Hkv;
     const int G = a.Hq / a.Hkv;
-    const int hs = w % a.HW, rs = w / a.HW;
+    const int hs = slot % a.HW, rs = slot / a.HW;
     const int h = g * G + hg * a.HW + hs;
     const int row0_wg = mb * (WR * RB);
     const int row0 = row0_wg + rs * WR;
@@ -92,191 +108,275 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     const int off = a.Nk - a.Nq;
     const int Nq = a.Nq, Nk = a.Nk;
 
-    // Key extent of the workgroup and of this wave.
+    // Key extents: workgroup, this slot, and keys every row of the slot sees.
     const int last_wg = min(row0_wg + WR * RB, Nq) - 1;
     const int kend_wg = CAUSAL ? min(Nk, last_wg + off + 1) : Nk;
-    const bool wave_live = row0 < Nq;
-    const int kend_w = !wave_live ? 0 : (CAUSAL ? min(Nk, min(row0 + WR, Nq) - 1 + off + 1) : Nk);
-    const int kfree_w = CAUSAL ? min(Nk, row0 + off + 1) : Nk;   // keys visible to all rows
+    const bool live = row0 < Nq;
+    const int kfree_w = CAUSAL ? min(Nk, row0 + off + 1) : Nk;
     const int ntiles = (kend_wg + BC - 1) / BC;
 
-    // Q rows of this lane, kept in registers (B operand of S^T = K Q^T).
+    // Q rows of this lane (B operand of S^T = K Q^T).
     V8 qf[KSTEPS];
     {
+        const int qrow = min(qi, Nq - 1);
         const S *qp = reinterpret_cast<const S *>(a.q) +
-                      ((size_t)((size_t)b * Nq + qi) * a.Hq + h) * D + 8 * lh;
+                      ((size_t)((size_t)b * Nq + qrow) * a.Hq + h) * D + 8 * lh;
 #pragma unroll
         for (int ks = 0; ks < KSTEPS; ++ks) {
-            uint4_t u = {0u, 0u, 0u, 0u};
-            if (qi < Nq) u = ld16(qp + 16 * ks);
+            uint4_t u = ld16(qp + 16 * ks);
             u ^= a.qsign;
             qf[ks] = as_vec8<V8>(u);
         }
     }
 
-    // Global tile loads: chunk c = tid + 256 i covers key c / CPR, column
-    // chunk c % CPR (consecutive threads read consecutive 16-byte pieces).
-    const S *kbase = reinterpret_cast<const S *>(a.k);
-    const S *vbase = reinterpret_cast<const S *>(a.v);
-    uint4_t kr[LOADS], vr[LOADS];
-    auto gload = [&](int kb) {
+    // Tile staging.  Waves 0-3 copy K rows (chunk c = tid + 256 i: key c / CPR,
+    // 16-byte column chunk c % CPR).  Waves 4-7 stage V transposed: unit u
+    // holds keys 2p, 2p+1 (p = u % 32) of column chunk u / 32 and writes eight
+    // 32-bit words, each the (2p, 2p+1) pair of one column d, into row d of V^T
+    // (as fp16).  Within every 16 keys the V^T positions swap bits 2 and 3 of
+    // the key index, so that the eight keys one MFMA lane needs are contiguous.
+    // Global addresses advance by one tile per step; only a tile that reaches
+    // past the last key recomputes them with the row index clamped (those keys
+    // are masked).
+    constexpr int SL = 16 * D / NT;             // 16-byte loads per thread per tile
+    const S *kvbase = reinterpret_cast<const S *>(kgroup_of(tid) ? a.k : a.v) +
+                      ((size_t)b * Nk * a.Hkv + g) * D;
+    const bool kgroup = kgroup_of(tid);
+    const int st = kgroup ? tid : tid - NT / 2;
+    const size_t row_elems = (size_t)a.Hkv * D;      // elements between consecutive keys
+    // tile-relative key and column of load i of this thread
+    auto lkey = [&](int i) {
+        return kgroup ? (st + (NT / 2) * i) / CPR : 2 * ((st + (NT / 2) * (i >> 1)) % 32) + (i & 1);
+    };
+    auto lcol = [&](int i) {
+        return kgroup ? 8 * ((st + (NT / 2) * i) % CPR) : 8 * ((st + (NT / 2) * (i >> 1)) / 32);
+    };
+    unsigned goff[SL];                               // tile-relative element offsets
 #pragma unroll
-        for (int i = 0; i < LOADS; ++i) {
-            const int c = tid + 256 * i;
-            const int key = kb + c / CPR, cc = c % CPR;
-            kr[i] = uint4_t{0u, 0u, 0u, 0u};
-            vr[i] = uint4_t{0u, 0u, 0u, 0u};
-            if (key < Nk) {
-                const size_t o = ((size_t)((size_t)b * Nk + key) * a.Hkv + g) * D + 8 * cc;
-                kr[i] = ld16(kbase + o);
-                vr[i] = ld16(vbase + o);
+    for (int i = 0; i < SL; ++i) goff[i] = (unsigned)(lkey(i) * row_elems + lcol(i));
+    uint4_t sr[SL];
+    auto gload = [&](int kb) {   // tile starting at key kb (called for kb = 0, 64, 128, ...)
+        if (kb + BC <= Nk) {
+            const S *tb = kvbase + (size_t)kb * row_elems;
+#pragma unroll
+            for (int i = 0; i < SL; ++i) sr[i] = ld16(tb + goff[i]);
+        } else {
+#pragma unroll
+            for (int i = 0; i < SL; ++i)
+                sr[i] = ld16(kvbase + (size_t)min(kb + lkey(i), Nk - 1) * row_elems + lcol(i));
+        }
+    };
+    // LDS destination (element offset inside a stage) of load i
+    auto sdst = [&](int i) {
+        if (kgroup) return lkey(i) * SM::KS + lcol(i);
+        const int key = lkey(i) & ~1;
+        const int pos = (key & ~12) | ((key & 4) << 1) | ((key & 8) >> 1);
+        return SM::KSZ + lcol(i) * SM::VTS + pos;   // row d = lcol + e, position pos
+    };
+    auto sstore = [&](unsigned short *stage) {
+        if (kgroup) {
+#pragma unroll
+            for (int i = 0; i < SL; ++i) st16(stage + sdst(i), sr[i]);
+        } else {
+#pragma unroll
+            for (int u = 0; u < SL / 2; ++u) {
+                unsigned *vt = reinterpret_cast<unsigned *>(stage + sdst(2 * u));
+                const uint4_t x = sr[2 * u], y = sr[2 * u + 1];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const unsigned xe = x[e >> 1], ye = y[e >> 1];
+                    unsigned w;
+                    if constexpr (IN_BF16) {
+                        const float fx = __uint_as_float((e & 1) ? (xe & 0xffff0000u) : (xe << 16));
+                        const float fy = __uint_as_float((e & 1) ? (ye & 0xffff0000u) : (ye << 16));
+                        w = pack_f16x2(fx, fy);
+                    } else {
+                        w = (e & 1) ? __builtin_amdgcn_perm(ye, xe, 0x07060302u)
+                                    : __builtin_amdgcn_perm(ye, xe, 0x05040100u);
+                    }
+                    vt[e * (SM::VTS / 2)] = w;
+                }
             }
         }
     };
-    auto sstore = [&](int buf) {
-        unsigned short *ks = smem + buf * SM::STAGE;
-        unsigned short *vs = ks + SM::KSZ;
-#pragma unroll
-        for (int i = 0; i < LOADS; ++i) {
-            const int c = tid + 256 * i;
-            const int key = c / CPR, cc = c % CPR;
-            st16(ks + key * SM::KS + 8 * cc, kr[i]);
-            st16(vs + key * SM::VS + 8 * cc, IN_BF16 ? bf16x8_to_f16x8(vr[i]) : vr[i]);
-        }
-    };
 
-    // Running state of this lane's query row (shared with lane l^32).
     float16_t oacc[DT];
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) oacc[dt] = float16_t{};
-    float m_run = -INFINITY;   // exponent base (log2 domain)
+    float m_run = -INFINITY;   // exponent base (log2 domain), same in lanes l and l^32
     float l_run = 0.f;         // this lane's part of the row sum
 
-    // Per-lane offsets into a stage.
-    const int k_lane = lq * SM::KS + 8 * lh;
-    const int v_lane = ((l & 15) >> 2) * SM::VS + 16 * ((l >> 4) & 1) + 4 * (l & 3) + 4 * lh * SM::VS;
+    const int k_lane = (32 * kh + lq) * SM::KS + 8 * lh;
+    const int v_lane = SM::KSZ + lq * SM::VTS + 32 * kh + 8 * lh;
 
+    // S^T = K Q^T for this wave's 32 keys of the tile held in `stage`
+    auto scores = [&](const unsigned short *stage) {
+        V8 ka[KSTEPS];
+#pragma unroll
+        for (int kk = 0; kk < KSTEPS; ++kk)
+            ka[kk] = as_vec8<V8>(*reinterpret_cast<const uint4_t *>(stage + k_lane + 16 * kk));
+        float16_t s = float16_t{};
+#pragma unroll
+        for (int kk = 0; kk < KSTEPS; ++kk) s = mfma32(ka[kk], qf[kk], s);
+        return s;
+    };
+
+    // Software pipeline: the scores of tile t + 1 are issued on the matrix
+    // cores while the softmax of tile t runs on the vector ALUs.  LDS holds
+    // three stages: V of tile t, K of tile t + 1, and tile t + 2 being written.
+    // Stage indices are compile-time constants (the loop is unrolled by three).
     if (ntiles > 0) {
         gload(0);
-        sstore(0);
+        sstore(smem);
+        if (ntiles > 1) {
+            gload(BC);
+            sstore(smem + SM::STAGE);
+        }
     }
     __syncthreads();
+    float16_t s = float16_t{};
+    if (ntiles > 0) s = scores(smem);
 
-    for (int t = 0; t < ntiles; ++t) {
+    // One tile: `cur` holds tile t, `nxt` tile t + 1, `fill` receives tile t + 2.
+    auto step = [&](int t, unsigned short *cur, unsigned short *nxt, unsigned short *fill,
+                    auto has_next) {
+        constexpr bool NEXT = decltype(has_next)::value;
         const int kb = t * BC;
-        if (t + 1 < ntiles) gload(kb + BC);
-        if (kb < kend_w) {
-            const unsigned short *ks = smem + (t & 1) * SM::STAGE;
-            const _Float16 *vs = reinterpret_cast<const _Float16 *>(ks + SM::KSZ);
-            // ---- S^T = K Q^T for two 32-key halves of the tile
-            float16_t s0 = float16_t{}, s1 = float16_t{};
+        const int kw = kb + 32 * kh;            // first key of this wave's half
+        const bool more = t + 2 < ntiles;
+        if (more) gload(kb + 2 * BC);
+        // V^T operands of tile t: row d = 32 dt + lane % 32, eight keys per k-step
+        half8_t va[DT][2];
 #pragma unroll
-            for (int kk = 0; kk < KSTEPS; ++kk) {
-                V8 a0 = as_vec8<V8>(*reinterpret_cast<const uint4_t *>(ks + k_lane + 16 * kk));
-                V8 a1 = as_vec8<V8>(
-                    *reinterpret_cast<const uint4_t *>(ks + k_lane + 32 * SM::KS + 16 * kk));
-                s0 = mfma32(a0, qf[kk], s0);
-                s1 = mfma32(a1, qf[kk], s1);
-            }
-            // ---- mask (only tiles that reach past the keys every row sees)
-            const bool masked = kb + BC > kfree_w;
-            if (masked) {
+        for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int key0 = kb + 8 * (r >> 2) + 4 * lh + (r & 3);
-                    const int key1 = key0 + 32;
-                    const bool v0 = key0 < Nk && (!CAUSAL || key0 <= qi + off);
-                    const bool v1 = key1 < Nk && (!CAUSAL || key1 <= qi + off);
-                    s0[r] = v0 ? s0[r] : -INFINITY;
-                    s1[r] = v1 ? s1[r] : -INFINITY;
-                }
-            }
-            // ---- row maximum of the tile (raw scores; c >= 0)
-            float mx = -INFINITY;
-#pragma unroll
-            for (int r = 0; r < 8; ++r) mx = max3(mx, s0[2 * r], s0[2 * r + 1]);
-#pragma unroll
-            for (int r = 0; r < 8; ++r) mx = max3(mx, s1[2 * r], s1[2 * r + 1]);
-            mx = pair_max(mx);
-            const float m_tile = (mx == -INFINITY) ? -INFINITY : mx * a.c;
-            // ---- lazy rescale of accumulator and sum
-            const float m_new = __builtin_fmaxf(m_run, m_tile);
-            const bool need = m_new > m_run + TAU;
-            if (__builtin_amdgcn_ballot_w64(need)) {
-                const float m_next = need ? m_new : m_run;
-                const float alpha = need ? exp2_fast(m_run - m_next) : 1.f;
-                m_run = m_next;
-                l_run *= alpha;
-#pragma unroll
-                for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
-            }
-            const float base = (m_run == -INFINITY) ? 0.f : m_run;
-            // ---- probabilities, row sum, fp16 operands for P V
-            float lsum = 0.f;
+            for (int j = 0; j < 2; ++j)
+                va[dt][j] = as_vec8<half8_t>(*reinterpret_cast<const uint4_t *>(
+                    cur + v_lane + 32 * dt * SM::VTS + 16 * j));
+        // mask only where some key of the half is hidden from some row
+        if (kw + 32 > kfree_w) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                float p0 = exp2_fast(__builtin_fmaf(s0[r], a.c, -base));
-                float p1 = exp2_fast(__builtin_fmaf(s1[r], a.c, -base));
-                if (masked) {
-                    p0 = (s0[r] == -INFINITY) ? 0.f : p0;
-                    p1 = (s1[r] == -INFINITY) ? 0.f : p1;
-                }
-                s0[r] = p0;
-                s1[r] = p1;
-                lsum += p0 + p1;
-            }
-            l_run += lsum;
-            half8_t pf[4];
-            pf[0] = pack_f16x8(s0[0], s0[1], s0[2], s0[3], s0[4], s0[5], s0[6], s0[7]);
-            pf[1] = pack_f16x8(s0[8], s0[9], s0[10], s0[11], s0[12], s0[13], s0[14], s0[15]);
-            pf[2] = pack_f16x8(s1[0], s1[1], s1[2], s1[3], s1[4], s1[5], s1[6], s1[7]);
-            pf[3] = pack_f16x8(s1[8], s1[9], s1[10], s1[11], s1[12], s1[13], s1[14], s1[15]);
-            // ---- O^T += V^T P^T; k-step j covers keys 16 j .. 16 j + 15 of the tile
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt) {
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const _Float16 *vp = vs + v_lane + 16 * j * SM::VS + 32 * dt;
-                    half8_t va = cat_half8(lds_read_tr16(vp), lds_read_tr16(vp + 8 * SM::VS));
-                    oacc[dt] = mfma32(va, pf[j], oacc[dt]);
-                }
+                const int key = kw + 8 * (r >> 2) + 4 * lh + (r & 3);
+                const bool vis = key < Nk && (!CAUSAL || key <= qi + off);
+                s[r] = vis ? s[r] : -INFINITY;
             }
         }
-        if (t + 1 < ntiles) sstore((t + 1) & 1);
+        // row maximum (raw scores; the exponent factor is positive)
+        float mx = max3(s[0], s[1], s[2]);
+        mx = max3(mx, s[3], s[4]);
+        mx = max3(mx, s[5], s[6]);
+        mx = max3(mx, s[7], s[8]);
+        mx = max3(mx, s[9], s[10]);
+        mx = max3(mx, s[11], s[12]);
+        mx = max3(mx, s[13], s[14]);
+        mx = __builtin_fmaxf(mx, s[15]);
+        mx = pair_max(mx);
+        const float m_new = __builtin_fmaxf(m_run, mx * a.c);
+        const bool need = m_new > m_run + TAU;
+        if (__builtin_amdgcn_ballot_w64(need)) {
+            const float m_next = need ? m_new : m_run;
+            const float alpha = need ? exp2_fast(m_run - m_next) : 1.f;
+            m_run = m_next;
+            l_run *= alpha;
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
+        }
+        const float nbase = (m_run == -INFINITY) ? 0.f : -m_run;
+        // next tile's scores on the matrix cores, this tile's exp on the VALU
+        float16_t s_next = float16_t{};
+        if constexpr (NEXT && PIPE) s_next = scores(nxt);
+        float p[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) p[r] = exp2_fast(__builtin_fmaf(s[r], a.c, nbase));
+        l_run += (((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]))) +
+                 (((p[8] + p[9]) + (p[10] + p[11])) + ((p[12] + p[13]) + (p[14] + p[15])));
+        const half8_t p0 = pack_f16x8(p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]);
+        const half8_t p1 = pack_f16x8(p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]);
+        // O^T += V^T P^T (k-step j = keys 16 j .. 16 j + 15 of the half)
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+            oacc[dt] = mfma32(va[dt][0], p0, oacc[dt]);
+            oacc[dt] = mfma32(va[dt][1], p1, oacc[dt]);
+        }
+        if (more) sstore(fill);
         __syncthreads();
+        if constexpr (NEXT) s = PIPE ? s_next : scores(nxt);
+    };
+    unsigned short *const s0 = smem, *const s1 = smem + SM::STAGE, *const s2 = smem + 2 * SM::STAGE;
+    int t = 0;
+    if constexpr (D == 64) {
+        // unrolled by three so that every stage offset is a constant
+        for (; t + 3 < ntiles; t += 3) {
+            step(t, s0, s1, s2, std::true_type{});
+            step(t + 1, s1, s2, s0, std::true_type{});
+            step(t + 2, s2, s0, s1, std::true_type{});
+        }
+    }
+    for (; t + 1 < ntiles; ++t) {
+        const int r = t % NSTAGE;
+        step(t, smem + r * SM::STAGE, smem + ((r + 1) % NSTAGE) * SM::STAGE,
+             smem + ((r + 2) % NSTAGE) * SM::STAGE, std::true_type{});
+    }
+    if (t < ntiles) {
+        const int r = t % NSTAGE;
+        step(t, smem + r * SM::STAGE, smem + ((r + 1) % NSTAGE) * SM::STAGE,
+             smem + ((r + 2) % NSTAGE) * SM::STAGE, std::false_type{});
     }
 
-    if (!wave_live) return;
-    // ---- final normalisation and stores
+    // ---- merge the two key halves of each slot through LDS
+    float *mf = reinterpret_cast<float *>(smem);
+    constexpr int NV = DT * 16 + 2;
+    float *mine = mf + (slot * NV) * 64 + l;
+    if (kh == 1) {
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) mine[(dt * 16 + r) * 64] = oacc[dt][r];
+        mine[(DT * 16) * 64] = m_run;
+        mine[(DT * 16 + 1) * 64] = l_run;
+    }
+    __syncthreads();
+    if (kh == 1 || !live) return;
+    {
+        const float m1 = mine[(DT * 16) * 64];
+        const float l1 = mine[(DT * 16 + 1) * 64];
+        const float M = __builtin_fmaxf(m_run, m1);
+        const float a0 = (m_run == -INFINITY) ? 0.f : exp2_fast(m_run - M);
+        const float a1 = (m1 == -INFINITY) ? 0.f : exp2_fast(m1 - M);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                oacc[dt][r] = a0 * oacc[dt][r] + a1 * mine[(dt * 16 + r) * 64];
+        l_run = a0 * l_run + a1 * l1;
+        m_run = M;
+    }
     const float l_tot = pair_sum(l_run);
     const float inv = 1.f / l_tot;
     if (qi < Nq) {
-        typedef TOUT OT;
-        OT *op = reinterpret_cast<OT *>(a.o) + ((size_t)((size_t)b * Nq + qi) * a.Hq + h) * D;
+        TOUT *op = reinterpret_cast<TOUT *>(a.o) + ((size_t)((size_t)b * Nq + qi) * a.Hq + h) * D;
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int d0 = 32 * dt + 8 * i + 4 * lh;
-                OT vals[4];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) vals[e] = from_f32<OT>(oacc[dt][4 * i + e] * inv);
-                if constexpr (sizeof(OT) == 4) {
+                if constexpr (sizeof(TOUT) == 4) {
                     *reinterpret_cast<float4_t *>(op + d0) =
-                        float4_t{vals[0], vals[1], vals[2], vals[3]};
+                        float4_t{oacc[dt][4 * i] * inv, oacc[dt][4 * i + 1] * inv,
+                                 oacc[dt][4 * i + 2] * inv, oacc[dt][4 * i + 3] * inv};
                 } else {
-                    typedef unsigned short us4 __attribute__((ext_vector_type(4)));
-                    us4 u;
+                    typedef TOUT t4 __attribute__((ext_vector_type(4)));
+                    t4 u;
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) u[e] = __builtin_bit_cast(unsigned short, vals[e]);
-                    *reinterpret_cast<us4 *>(op + d0) = u;
+                    for (int e = 0; e < 4; ++e) u[e] = from_f32<TOUT>(oacc[dt][4 * i + e] * inv);
+                    *reinterpret_cast<t4 *>(op + d0) = u;
                 }
             }
         }
         if (a.lse && lh == 0)
             a.lse[((size_t)b * a.Hq + h) * Nq + qi] = (m_run + log2f(l_tot)) * kLn2;
     }
-    (void)a.scale_zero;
 }
 
 template <typename TIN, typename TOUT, int D, bool CAUSAL>
@@ -284,19 +384,20 @@ hipError_t launch_t(const Problem &p, hipStream_t stream) {
     PrefillArgs a;
     a.q = p.q; a.k = p.k; a.v = p.v; a.o = p.o; a.lse = p.lse;
     a.B = p.B; a.Hq = p.Hq; a.Hkv = p.Hkv; a.Nq = p.Nq; a.Nk = p.Nk;
-    a.c = __builtin_fabsf(p.scale) * kLog2e;
-    a.scale_zero = p.scale == 0.f ? 1.f : 0.f;
+    // A zero scale keeps a tiny positive factor: every visible exponent is then
+    // exactly 0 in fp32, and masked (-inf) scores still give 0.
+    a.c = __builtin_fmaxf(__builtin_fabsf(p.scale), 1e-30f) * kLog2e;
     a.qsign = p.scale < 0.f ? 0x80008000u : 0u;
     const int G = p.Hq / p.Hkv;
-    a.HW = (G % 4 == 0) ? 4 : (G % 2 == 0 ? 2 : 1);
-    const int RB = NW / a.HW;
+    a.HW = (NSLOT % 4 == 0 && G % 4 == 0) ? 4 : (G % 2 == 0 ? 2 : 1);
+    const int RB = NSLOT / a.HW;
     a.nmb = (p.Nq + WR * RB - 1) / (WR * RB);
     a.nhg = G / a.HW;
     const long long nblocks = (long long)a.nmb * p.B * p.Hkv * a.nhg;
     if (nblocks <= 0) return hipSuccess;
     if (nblocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL((prefill_kernel<TIN, TOUT, D, CAUSAL>), dim3((unsigned)nblocks),
-                       dim3(256), 0, stream, a);
+    hipLaunchKernelGGL((prefill_kernel<TIN, TOUT, D, CAUSAL>), dim3((unsigned)nblocks), dim3(NT),
+                       0, stream, a);
     return hipGetLastError();
 }
 

@@ -187,3 +187,17 @@ def test_values_near_fp16_range_in_bf16_inputs():
     og = to_np(o)
     rel = np.abs(og - o_ref).max() / np.abs(o_ref).max()
     assert np.isfinite(og).all() and rel < 1e-3
+
+
+def test_decode_calls_with_changing_shapes():
+    """Consecutive decode calls with different batch / head layouts and split
+    counts share the library's buffers; each must still match the oracle."""
+    shapes = [(16, 32, 8, 1000, 128, "bf16", 4), (8, 16, 1, 3001, 64, "f16", 8),
+              (2, 64, 2, 700, 128, "bf16", 3), (16, 32, 8, 1000, 128, "bf16", 4),
+              (1, 16, 16, 2000, 64, "f16", 0), (8, 16, 1, 3001, 64, "f16", 8)]
+    for i, (B, Hq, Hkv, Nk, D, dt, S) in enumerate(shapes):
+        q, k, v = make_qkv(B, Hq, Hkv, 1, Nk, D, dt, seed=500 + i)
+        o_ref, l_ref = oracle.attention(q, k, v, False, default_scale(D))
+        o, lse = gpu_attention(q, k, v, False, default_scale(D), out_dtype=torch.float32,
+                               num_splits=S)
+        check_against(o, lse, o_ref, l_ref, DTYPES[dt], True, f"call {i} {B}x{Hq}x{Hkv}")
