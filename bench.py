@@ -205,6 +205,16 @@ def main():
             extras.append({"workload": name, "us_per_call": round(xms * 1e3, 2),
                            "value": round(val, 2), "unit": u, "frac": round(val / pk, 4),
                            "steps": steps})
+            if name == "gqa_decode_bf16":
+                result["decode"] = {
+                    "workload": name, "metric": "decode KV GB/s (K+V bytes read once)",
+                    "value": round(val, 1), "unit": "GB/s", "us_per_call": round(xms * 1e3, 2),
+                    "roofline": {"bound": "hbm", "achieved": round(val, 1), "peak": PEAK_HBM_GBS,
+                                 "unit": "GB/s", "frac": round(val / PEAK_HBM_GBS, 4),
+                                 "traffic": stored_traffic("decode_split_kernel", name,
+                                                           DECODE_SOURCES),
+                                 "kernel": "decode_split_kernel + decode_combine_kernel",
+                                 "algorithmic_per_launch": x.kv_bytes()}}
             log(f"[bench] {name}: {xms * 1e3:.1f} us/call, {val:.1f} {u} ({100 * val / pk:.1f}%)")
             torch.cuda.empty_cache()
         # achievable HBM bandwidth for context: a plain 1 GiB device copy

@@ -1,0 +1,43 @@
+"""Minimal runs for profilers (rocprofv3): one workload's attention call a few
+times, or a plain device copy of known size (the reference for scaling the
+HBM byte counters).
+
+    python3 paper_2608_18656_amd/profile_run.py gqa_prefill_bf16 5
+    python3 paper_2608_18656_amd/profile_run.py copy 268435456 5
+"""
+from __future__ import annotations
+
+import os
+import sys
+
+sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+
+
+def main(argv):
+    import torch
+
+    what = argv[1] if len(argv) > 1 else "gqa_prefill_bf16"
+    if what == "copy":
+        nbytes = int(argv[2]) if len(argv) > 2 else 1 << 28
+        reps = int(argv[3]) if len(argv) > 3 else 5
+        src = torch.ones(nbytes // 2, dtype=torch.float16, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(reps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"copied {nbytes} bytes x {reps}", flush=True)
+        return
+    import paper_2608_18656_amd as fa
+    from paper_2608_18656_amd.inputs import WORKLOADS, make_workload
+
+    reps = int(argv[2]) if len(argv) > 2 else 5
+    w = WORKLOADS[what]
+    q, k, v = (t.cuda() for t in make_workload(w))
+    for _ in range(reps):
+        fa.fwd(q, k, v, causal=w.causal, scale=w.softmax_scale)
+    torch.cuda.synchronize()
+    print(f"ran {what} x {reps}", flush=True)
+
+
+if __name__ == "__main__":
+    main(sys.argv)
