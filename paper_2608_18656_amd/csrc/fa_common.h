@@ -19,6 +19,8 @@
 namespace fa {
 
 typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef short short4_t __attribute__((ext_vector_type(4)));
 typedef float float16_t __attribute__((ext_vector_type(16)));
@@ -86,7 +88,6 @@ __device__ __forceinline__ uint4_t bf16x8_to_f16x8(uint4_t u) {
 
 // Two fp32 values -> packed f16 pair (first in the low half), round to nearest even.
 __device__ __forceinline__ unsigned pack_f16x2(float lo, float hi) {
-    typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
     half2_t h;
     h[0] = (_Float16)lo;
     h[1] = (_Float16)hi;
@@ -100,6 +101,19 @@ __device__ __forceinline__ half8_t pack_f16x8(float a0, float a1, float a2, floa
     h[0] = (_Float16)a0; h[1] = (_Float16)a1; h[2] = (_Float16)a2; h[3] = (_Float16)a3;
     h[4] = (_Float16)a4; h[5] = (_Float16)a5; h[6] = (_Float16)a6; h[7] = (_Float16)a7;
     return h;
+}
+
+// Sum of 16 f16 values (two f16 x8 words) accumulated in fp32 (dot products
+// with (1, 1), two independent chains).
+__device__ __forceinline__ float sum_f16x16(half8_t a, half8_t b) {
+    const half2_t one = {(_Float16)1.0f, (_Float16)1.0f};
+    float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        s0 = __builtin_amdgcn_fdot2(half2_t{a[2 * i], a[2 * i + 1]}, one, s0, false);
+        s1 = __builtin_amdgcn_fdot2(half2_t{b[2 * i], b[2 * i + 1]}, one, s1, false);
+    }
+    return s0 + s1;
 }
 
 // Reductions over the lane pair (l, l^32).  v_permlane32_swap exchanges the

@@ -42,7 +42,7 @@ constexpr int BC = 64;        // keys per tile (two halves of 32, one per wave)
 constexpr int WR = 32;        // query rows per slot
 constexpr int NSLOT = 4;      // slots per workgroup
 constexpr int NT = 128 * NSLOT;   // threads per workgroup (two waves per slot)
-constexpr float TAU = 8.0f;   // lazy-rescale threshold (log2 units)
+constexpr float kMaxLaneSum = 4096.0f;   // largest 16-weight lane sum kept without a rescale
 constexpr int NSTAGE = 3;     // LDS tile stages
 
 struct PrefillArgs {
@@ -80,15 +80,12 @@ __global__ __launch_bounds__(NT, 1) void prefill_kernel(PrefillArgs a) {
     constexpr int LOADS = BC * D / 8 / NT;  // 16-byte chunks per thread per K (or V) tile
     constexpr int CPR = D / 8;              // 16-byte chunks per row
     constexpr bool IN_BF16 = __is_same(TIN, bf16_t);
-    // Issue the next tile's scores during this tile's softmax (D = 64, where
-    // the vector ALU work is as large as the matrix work); at D = 128 the
-    // registers are needed for the larger accumulator instead.
-    constexpr bool PIPE = D == 64;
 
     __shared__ __attribute__((aligned(16))) unsigned short smem[SM::WORDS];
 
     const int tid = threadIdx.x;
-    const int w = tid >> 6, l = tid & 63, lq = l & 31, lh = l >> 5;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int l = tid & 63, lq = l & 31, lh = l >> 5;
     const int kh = w / NSLOT, slot = w % NSLOT;
     const int RB = NSLOT / a.HW;
     const int per_mb = a.B * a.Hkv * a.nhg;
@@ -205,6 +202,7 @@ __global__ __launch_bounds__(NT, 1) void prefill_kernel(PrefillArgs a) {
     for (int dt = 0; dt < DT; ++dt) oacc[dt] = float16_t{};
     float m_run = -INFINITY;   // exponent base (log2 domain), same in lanes l and l^32
     float l_run = 0.f;         // this lane's part of the row sum
+    bool fresh = true;         // some row of the wave has no base yet (wave-uniform)
 
     const int k_lane = (32 * kh + lq) * SM::KS + 8 * lh;
     const int v_lane = SM::KSZ + lq * SM::VTS + 32 * kh + 8 * lh;
@@ -221,38 +219,27 @@ __global__ __launch_bounds__(NT, 1) void prefill_kernel(PrefillArgs a) {
         return s;
     };
 
-    // Software pipeline: the scores of tile t + 1 are issued on the matrix
-    // cores while the softmax of tile t runs on the vector ALUs.  LDS holds
-    // three stages: V of tile t, K of tile t + 1, and tile t + 2 being written.
-    // Stage indices are compile-time constants (the loop is unrolled by three).
-    if (ntiles > 0) {
-        gload(0);
-        sstore(smem);
-        if (ntiles > 1) {
-            gload(BC);
-            sstore(smem + SM::STAGE);
-        }
-    }
-    __syncthreads();
-    float16_t s = float16_t{};
-    if (ntiles > 0) s = scores(smem);
+    // p = 2^(s c - m) for the 16 scores of the lane, packed to f16 in the
+    // key order of the two PV k-steps
+    auto exp_pack = [&](const float16_t &s, float nbase, half8_t &p0, half8_t &p1) {
+        float p[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) p[r] = exp2_fast(__builtin_fmaf(s[r], a.c, nbase));
+        p0 = pack_f16x8(p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]);
+        p1 = pack_f16x8(p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]);
+    };
 
-    // One tile: `cur` holds tile t, `nxt` tile t + 1, `fill` receives tile t + 2.
-    auto step = [&](int t, unsigned short *cur, unsigned short *nxt, unsigned short *fill,
-                    auto has_next) {
-        constexpr bool NEXT = decltype(has_next)::value;
-        const int kb = t * BC;
-        const int kw = kb + 32 * kh;            // first key of this wave's half
-        const bool more = t + 2 < ntiles;
-        if (more) gload(kb + 2 * BC);
-        // V^T operands of tile t: row d = 32 dt + lane % 32, eight keys per k-step
-        half8_t va[DT][2];
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-            for (int j = 0; j < 2; ++j)
-                va[dt][j] = as_vec8<half8_t>(*reinterpret_cast<const uint4_t *>(
-                    cur + v_lane + 32 * dt * SM::VTS + 16 * j));
+    // Online softmax and O^T += V^T P^T for the scores `s` of tile t (this
+    // wave's 32 keys of it), V^T read from `stage`.  Fast path: exponentiate
+    // against the current base and keep the weights if each lane's sum of its
+    // 16 weights stays at most 4096 (so every weight fits f16 with room to
+    // spare, and the accumulator needs no rescale); the row maximum is never
+    // formed.  Only when some row outgrows its base that far (or a row has no
+    // base yet) is the row maximum taken, the accumulator rescaled to it and
+    // the weights recomputed.  The row sum adds, in fp32, the f16 weights that
+    // also feed the matrix product.
+    auto softmax_pv = [&](float16_t s, int t, const unsigned short *stage) {
+        const int kw = t * BC + 32 * kh;        // first key of this wave's half
         // mask only where some key of the half is hidden from some row
         if (kw + 32 > kfree_w) {
 #pragma unroll
@@ -262,67 +249,106 @@ __global__ __launch_bounds__(NT, 1) void prefill_kernel(PrefillArgs a) {
                 s[r] = vis ? s[r] : -INFINITY;
             }
         }
-        // row maximum (raw scores; the exponent factor is positive)
-        float mx = max3(s[0], s[1], s[2]);
-        mx = max3(mx, s[3], s[4]);
-        mx = max3(mx, s[5], s[6]);
-        mx = max3(mx, s[7], s[8]);
-        mx = max3(mx, s[9], s[10]);
-        mx = max3(mx, s[11], s[12]);
-        mx = max3(mx, s[13], s[14]);
-        mx = __builtin_fmaxf(mx, s[15]);
-        mx = pair_max(mx);
-        const float m_new = __builtin_fmaxf(m_run, mx * a.c);
-        const bool need = m_new > m_run + TAU;
-        if (__builtin_amdgcn_ballot_w64(need)) {
-            const float m_next = need ? m_new : m_run;
-            const float alpha = need ? exp2_fast(m_run - m_next) : 1.f;
-            m_run = m_next;
+        half8_t p0, p1;
+        float ls = 0.f;
+        bool slow = fresh;
+        if (!slow) {
+            exp_pack(s, -m_run, p0, p1);
+            ls = sum_f16x16(p0, p1);
+            slow = __builtin_amdgcn_ballot_w64(!(ls <= kMaxLaneSum)) != 0;
+        }
+        if (slow) {
+            float mx = max3(s[0], s[1], s[2]);
+            mx = max3(mx, s[3], s[4]);
+            mx = max3(mx, s[5], s[6]);
+            mx = max3(mx, s[7], s[8]);
+            mx = max3(mx, s[9], s[10]);
+            mx = max3(mx, s[11], s[12]);
+            mx = max3(mx, s[13], s[14]);
+            mx = __builtin_fmaxf(mx, s[15]);
+            mx = pair_max(mx);
+            const float m_new = __builtin_fmaxf(m_run, mx * a.c);
+            const float alpha = (m_new == -INFINITY) ? 1.f : exp2_fast(m_run - m_new);
+            m_run = m_new;
             l_run *= alpha;
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
+            exp_pack(s, (m_run == -INFINITY) ? 0.f : -m_run, p0, p1);
+            ls = sum_f16x16(p0, p1);
+            fresh = __builtin_amdgcn_ballot_w64(m_run == -INFINITY) != 0;
         }
-        const float nbase = (m_run == -INFINITY) ? 0.f : -m_run;
-        // next tile's scores on the matrix cores, this tile's exp on the VALU
-        float16_t s_next = float16_t{};
-        if constexpr (NEXT && PIPE) s_next = scores(nxt);
-        float p[16];
-#pragma unroll
-        for (int r = 0; r < 16; ++r) p[r] = exp2_fast(__builtin_fmaf(s[r], a.c, nbase));
-        l_run += (((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]))) +
-                 (((p[8] + p[9]) + (p[10] + p[11])) + ((p[12] + p[13]) + (p[14] + p[15])));
-        const half8_t p0 = pack_f16x8(p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]);
-        const half8_t p1 = pack_f16x8(p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]);
+        l_run += ls;
         // O^T += V^T P^T (k-step j = keys 16 j .. 16 j + 15 of the half)
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
-            oacc[dt] = mfma32(va[dt][0], p0, oacc[dt]);
-            oacc[dt] = mfma32(va[dt][1], p1, oacc[dt]);
+            half8_t va[2];
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                va[j] = as_vec8<half8_t>(*reinterpret_cast<const uint4_t *>(
+                    stage + v_lane + 32 * dt * SM::VTS + 16 * j));
+            oacc[dt] = mfma32(va[0], p0, oacc[dt]);
+            oacc[dt] = mfma32(va[1], p1, oacc[dt]);
         }
-        if (more) sstore(fill);
-        __syncthreads();
-        if constexpr (NEXT) s = PIPE ? s_next : scores(nxt);
     };
-    unsigned short *const s0 = smem, *const s1 = smem + SM::STAGE, *const s2 = smem + 2 * SM::STAGE;
-    int t = 0;
-    if constexpr (D == 64) {
-        // unrolled by three so that every stage offset is a constant
-        for (; t + 3 < ntiles; t += 3) {
-            step(t, s0, s1, s2, std::true_type{});
-            step(t + 1, s1, s2, s0, std::true_type{});
-            step(t + 2, s2, s0, s1, std::true_type{});
+
+    // Tile loop.  The two waves of a slot share a SIMD and run the same steps
+    // half a tile apart: the leading wave (first key half) computes the scores,
+    // softmax and PV product of tile t in step t; the lagging wave first does
+    // softmax and PV for tile t - 1 (scores kept from the previous step), then
+    // the scores of tile t.  So while one wave is in its softmax (vector ALU)
+    // the other has matrix work queued, and the SIMD keeps both units busy.
+    // LDS holds three stages: tile t, tile t - 1 (V still read by the lagging
+    // wave) and tile t + 1 being written from the registers loaded this step.
+    if (ntiles > 0) {
+        gload(0);
+        sstore(smem);
+    }
+    __syncthreads();
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    auto stage_at = [&](int r) { return smem + r * SM::STAGE; };
+    if (kh == 0) {
+        // tile t lives in stage t % 3; the loop is unrolled by three so that
+        // every stage offset is a constant
+        auto step = [&](int t, auto R) {
+            constexpr int r = decltype(R)::value;
+            const bool more = t + 1 < ntiles;
+            if (more) gload((t + 1) * BC);
+            softmax_pv(scores(stage_at(r)), t, stage_at(r));
+            if (more) sstore(stage_at((r + 1) % NSTAGE));
+            __syncthreads();
+        };
+        int t = 0;
+        for (; t + 3 <= ntiles; t += 3) {
+            step(t, I0{});
+            step(t + 1, I1{});
+            step(t + 2, I2{});
         }
+        if (t < ntiles) step(t, I0{});
+        if (t + 1 < ntiles) step(t + 1, I1{});
+    } else if (ntiles > 0) {
+        float16_t s_lag;
+        auto step = [&](int t, auto R) {
+            constexpr int r = decltype(R)::value;
+            const bool more = t + 1 < ntiles;
+            if (more) gload((t + 1) * BC);
+            if (t > 0) softmax_pv(s_lag, t - 1, stage_at((r + NSTAGE - 1) % NSTAGE));
+            s_lag = scores(stage_at(r));
+            if (more) sstore(stage_at((r + 1) % NSTAGE));
+            __syncthreads();
+        };
+        int t = 0;
+        for (; t + 3 <= ntiles; t += 3) {
+            step(t, I0{});
+            step(t + 1, I1{});
+            step(t + 2, I2{});
+        }
+        if (t < ntiles) step(t, I0{});
+        if (t + 1 < ntiles) step(t + 1, I1{});
+        softmax_pv(s_lag, ntiles - 1, stage_at((ntiles - 1) % NSTAGE));
     }
-    for (; t + 1 < ntiles; ++t) {
-        const int r = t % NSTAGE;
-        step(t, smem + r * SM::STAGE, smem + ((r + 1) % NSTAGE) * SM::STAGE,
-             smem + ((r + 2) % NSTAGE) * SM::STAGE, std::true_type{});
-    }
-    if (t < ntiles) {
-        const int r = t % NSTAGE;
-        step(t, smem + r * SM::STAGE, smem + ((r + 1) % NSTAGE) * SM::STAGE,
-             smem + ((r + 2) % NSTAGE) * SM::STAGE, std::false_type{});
-    }
+    __syncthreads();   // the merge below reuses the stage memory
 
     // ---- merge the two key halves of each slot through LDS
     float *mf = reinterpret_cast<float *>(smem);
