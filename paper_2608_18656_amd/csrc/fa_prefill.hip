@@ -43,7 +43,7 @@ constexpr int WR = 32;        // query rows per slot
 constexpr int NSLOT = 4;      // slots per workgroup
 constexpr int NT = 128 * NSLOT;   // threads per workgroup (two waves per slot)
 constexpr float kMaxLaneSum = 4096.0f;   // largest 16-weight lane sum kept without a rescale
-constexpr int NSTAGE = 3;     // LDS tile stages
+constexpr int NSTAGE = 4;     // LDS tile stages
 
 struct PrefillArgs {
     const void *q, *k, *v;
@@ -151,16 +151,19 @@ __global__ __launch_bounds__(NT, 1) void prefill_kernel(PrefillArgs a) {
     unsigned goff[SL];                               // tile-relative element offsets
 #pragma unroll
     for (int i = 0; i < SL; ++i) goff[i] = (unsigned)(lkey(i) * row_elems + lcol(i));
-    uint4_t sr[SL];
-    auto gload = [&](int kb) {   // tile starting at key kb (called for kb = 0, 64, 128, ...)
+    // Staging registers: NSET sets, so that a tile's global loads can be in
+    // flight for NSET steps before it is written to LDS.
+    constexpr int NSET = D == 64 ? 2 : 1;
+    uint4_t sr[NSET][SL];
+    auto gload = [&](int kb, int set) {   // tile starting at key kb (kb = 0, 64, 128, ...)
         if (kb + BC <= Nk) {
             const S *tb = kvbase + (size_t)kb * row_elems;
 #pragma unroll
-            for (int i = 0; i < SL; ++i) sr[i] = ld16(tb + goff[i]);
+            for (int i = 0; i < SL; ++i) sr[set][i] = ld16(tb + goff[i]);
         } else {
 #pragma unroll
             for (int i = 0; i < SL; ++i)
-                sr[i] = ld16(kvbase + (size_t)min(kb + lkey(i), Nk - 1) * row_elems + lcol(i));
+                sr[set][i] = ld16(kvbase + (size_t)min(kb + lkey(i), Nk - 1) * row_elems + lcol(i));
         }
     };
     // LDS destination (element offset inside a stage) of load i
@@ -170,15 +173,15 @@ __global__ __launch_bounds__(NT, 1) void prefill_kernel(PrefillArgs a) {
         const int pos = (key & ~12) | ((key & 4) << 1) | ((key & 8) >> 1);
         return SM::KSZ + lcol(i) * SM::VTS + pos;   // row d = lcol + e, position pos
     };
-    auto sstore = [&](unsigned short *stage) {
+    auto sstore = [&](unsigned short *stage, int set) {
         if (kgroup) {
 #pragma unroll
-            for (int i = 0; i < SL; ++i) st16(stage + sdst(i), sr[i]);
+            for (int i = 0; i < SL; ++i) st16(stage + sdst(i), sr[set][i]);
         } else {
 #pragma unroll
             for (int u = 0; u < SL / 2; ++u) {
                 unsigned *vt = reinterpret_cast<unsigned *>(stage + sdst(2 * u));
-                const uint4_t x = sr[2 * u], y = sr[2 * u + 1];
+                const uint4_t x = sr[set][2 * u], y = sr[set][2 * u + 1];
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
                     const unsigned xe = x[e >> 1], ye = y[e >> 1];
@@ -206,6 +209,7 @@ __global__ __launch_bounds__(NT, 1) void prefill_kernel(PrefillArgs a) {
 
     const int k_lane = (32 * kh + lq) * SM::KS + 8 * lh;
     const int v_lane = SM::KSZ + lq * SM::VTS + 32 * kh + 8 * lh;
+    auto stage_at = [&](int r) { return smem + r * SM::STAGE; };
 
     // S^T = K Q^T for this wave's 32 keys of the tile held in `stage`
     auto scores = [&](const unsigned short *stage) {
@@ -219,7 +223,35 @@ __global__ __launch_bounds__(NT, 1) void prefill_kernel(PrefillArgs a) {
         return s;
     };
 
-    // p = 2^(s c - m) for the 16 scores of the lane, packed to f16 in the
+    // O^T += V^T P^T with the weights of one tile (k-step j = keys 16 j .. 16 j
+    // + 15 of the wave's half), V^T read from `stage`
+    auto pv = [&](const half8_t &p0, const half8_t &p1, const unsigned short *stage) {
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+            half8_t va[2];
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                va[j] = as_vec8<half8_t>(*reinterpret_cast<const uint4_t *>(
+                    stage + v_lane + 32 * dt * SM::VTS + 16 * j));
+            oacc[dt] = mfma32(va[0], p0, oacc[dt]);
+            oacc[dt] = mfma32(va[1], p1, oacc[dt]);
+        }
+    };
+
+    // hide keys of tile t that some row of the wave must not see
+    auto mask = [&](float16_t &s, int t) {
+        const int kw = t * BC + 32 * kh;        // first key of this wave's half
+        if (kw + 32 > kfree_w) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int key = kw + 8 * (r >> 2) + 4 * lh + (r & 3);
+                const bool vis = key < Nk && (!CAUSAL || key <= qi + off);
+                s[r] = vis ? s[r] : -INFINITY;
+            }
+        }
+    };
+
+    // p = 2^(s c + nbase) for the 16 scores of the lane, packed to f16 in the
     // key order of the two PV k-steps
     auto exp_pack = [&](const float16_t &s, float nbase, half8_t &p0, half8_t &p1) {
         float p[16];
@@ -229,35 +261,15 @@ __global__ __launch_bounds__(NT, 1) void prefill_kernel(PrefillArgs a) {
         p1 = pack_f16x8(p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]);
     };
 
-    // Online softmax and O^T += V^T P^T for the scores `s` of tile t (this
-    // wave's 32 keys of it), V^T read from `stage`.  Fast path: exponentiate
-    // against the current base and keep the weights if each lane's sum of its
-    // 16 weights stays at most 4096 (so every weight fits f16 with room to
-    // spare, and the accumulator needs no rescale); the row maximum is never
-    // formed.  Only when some row outgrows its base that far (or a row has no
-    // base yet) is the row maximum taken, the accumulator rescaled to it and
-    // the weights recomputed.  The row sum adds, in fp32, the f16 weights that
-    // also feed the matrix product.
-    auto softmax_pv = [&](float16_t s, int t, const unsigned short *stage) {
-        const int kw = t * BC + 32 * kh;        // first key of this wave's half
-        // mask only where some key of the half is hidden from some row
-        if (kw + 32 > kfree_w) {
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int key = kw + 8 * (r >> 2) + 4 * lh + (r & 3);
-                const bool vis = key < Nk && (!CAUSAL || key <= qi + off);
-                s[r] = vis ? s[r] : -INFINITY;
-            }
-        }
-        half8_t p0, p1;
-        float ls = 0.f;
-        bool slow = fresh;
-        if (!slow) {
-            exp_pack(s, -m_run, p0, p1);
-            ls = sum_f16x16(p0, p1);
-            slow = __builtin_amdgcn_ballot_w64(!(ls <= kMaxLaneSum)) != 0;
-        }
-        if (slow) {
+    // Online softmax of one tile.  The weights are first formed against the
+    // current base and kept if each lane's sum of its 16 weights stays at most
+    // 4096 (every weight then fits f16 with room to spare and no rescale is
+    // due; the row maximum is never formed).  Only when some row outgrows its
+    // base that far (or a row has no base yet) is the row maximum taken, the
+    // accumulator and row sum rescaled to it and the weights recomputed.  The
+    // row sum adds, in fp32, the f16 weights that also feed the matrix product.
+    auto finish = [&](const float16_t &s, half8_t &p0, half8_t &p1, float ls, bool bad) {
+        if (__builtin_amdgcn_ballot_w64(bad) != 0) {
             float mx = max3(s[0], s[1], s[2]);
             mx = max3(mx, s[3], s[4]);
             mx = max3(mx, s[5], s[6]);
@@ -278,75 +290,70 @@ __global__ __launch_bounds__(NT, 1) void prefill_kernel(PrefillArgs a) {
             fresh = __builtin_amdgcn_ballot_w64(m_run == -INFINITY) != 0;
         }
         l_run += ls;
-        // O^T += V^T P^T (k-step j = keys 16 j .. 16 j + 15 of the half)
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-            half8_t va[2];
-#pragma unroll
-            for (int j = 0; j < 2; ++j)
-                va[j] = as_vec8<half8_t>(*reinterpret_cast<const uint4_t *>(
-                    stage + v_lane + 32 * dt * SM::VTS + 16 * j));
-            oacc[dt] = mfma32(va[0], p0, oacc[dt]);
-            oacc[dt] = mfma32(va[1], p1, oacc[dt]);
-        }
     };
 
-    // Tile loop.  The two waves of a slot share a SIMD and run the same steps
-    // half a tile apart: the leading wave (first key half) computes the scores,
-    // softmax and PV product of tile t in step t; the lagging wave first does
-    // softmax and PV for tile t - 1 (scores kept from the previous step), then
-    // the scores of tile t.  So while one wave is in its softmax (vector ALU)
-    // the other has matrix work queued, and the SIMD keeps both units busy.
-    // LDS holds three stages: tile t, tile t - 1 (V still read by the lagging
-    // wave) and tile t + 1 being written from the registers loaded this step.
+    half8_t pp0, pp1;   // weights of the previous tile
+
+    // Tile loop, software-pipelined inside each wave: step i computes the
+    // scores of tile i + 1 and the PV product of tile i - 1 on the matrix
+    // cores while the softmax of tile i runs on the vector ALU; the three
+    // streams are independent, so the scheduler interleaves them.  Tile j sits
+    // in LDS stage j % 4 from step j - 2 (written from registers loaded in that
+    // step, or at D = 64 in the step before) until its V is read in step j + 1.
     if (ntiles > 0) {
-        gload(0);
-        sstore(smem);
+        gload(0, 0);
+        sstore(stage_at(0), 0);
     }
+    if (ntiles > 1) {
+        gload(BC, 1 % NSET);
+        sstore(stage_at(1), 1 % NSET);
+    }
+    if (NSET == 2 && ntiles > 2) gload(2 * BC, 0);
     __syncthreads();
+    float16_t s_cur = scores(stage_at(0));
+    auto step = [&](int i, auto R, auto FIRST) {
+        constexpr int r = decltype(R)::value;
+        constexpr bool first = decltype(FIRST)::value;
+        const bool more = i + 2 < ntiles;
+        if (NSET == 2) {
+            if (i + 3 < ntiles) gload((i + 3) * BC, (r + 1) % 2);
+        } else if (more) {
+            gload((i + 2) * BC, 0);
+        }
+        mask(s_cur, i);
+        // independent work of the step: scores of tile i + 1 and PV of tile
+        // i - 1 on the matrix cores, softmax of tile i on the vector ALU
+        const float16_t s_next = scores(stage_at((r + 1) % NSTAGE));   // unused after the last tile
+        if constexpr (!first) pv(pp0, pp1, stage_at((r + NSTAGE - 1) % NSTAGE));
+        half8_t p0, p1;
+        exp_pack(s_cur, fresh ? 0.f : -m_run, p0, p1);
+        const float ls = sum_f16x16(p0, p1);
+        const bool bad = (!(ls <= kMaxLaneSum)) | fresh;
+        finish(s_cur, p0, p1, ls, bad);
+        pp0 = p0;
+        pp1 = p1;
+        s_cur = s_next;
+        if (more) sstore(stage_at((r + 2) % NSTAGE), r % NSET);
+        __syncthreads();
+    };
     using I0 = std::integral_constant<int, 0>;
     using I1 = std::integral_constant<int, 1>;
     using I2 = std::integral_constant<int, 2>;
-    auto stage_at = [&](int r) { return smem + r * SM::STAGE; };
-    if (kh == 0) {
-        // tile t lives in stage t % 3; the loop is unrolled by three so that
-        // every stage offset is a constant
-        auto step = [&](int t, auto R) {
-            constexpr int r = decltype(R)::value;
-            const bool more = t + 1 < ntiles;
-            if (more) gload((t + 1) * BC);
-            softmax_pv(scores(stage_at(r)), t, stage_at(r));
-            if (more) sstore(stage_at((r + 1) % NSTAGE));
-            __syncthreads();
-        };
-        int t = 0;
-        for (; t + 3 <= ntiles; t += 3) {
-            step(t, I0{});
-            step(t + 1, I1{});
-            step(t + 2, I2{});
+    using I3 = std::integral_constant<int, 3>;
+    if (ntiles > 0) {
+        step(0, I0{}, std::true_type{});
+        int i = 1;
+        // unrolled by four so that every stage offset is a constant
+        for (; i + 4 <= ntiles; i += 4) {
+            step(i, I1{}, std::false_type{});
+            step(i + 1, I2{}, std::false_type{});
+            step(i + 2, I3{}, std::false_type{});
+            step(i + 3, I0{}, std::false_type{});
         }
-        if (t < ntiles) step(t, I0{});
-        if (t + 1 < ntiles) step(t + 1, I1{});
-    } else if (ntiles > 0) {
-        float16_t s_lag;
-        auto step = [&](int t, auto R) {
-            constexpr int r = decltype(R)::value;
-            const bool more = t + 1 < ntiles;
-            if (more) gload((t + 1) * BC);
-            if (t > 0) softmax_pv(s_lag, t - 1, stage_at((r + NSTAGE - 1) % NSTAGE));
-            s_lag = scores(stage_at(r));
-            if (more) sstore(stage_at((r + 1) % NSTAGE));
-            __syncthreads();
-        };
-        int t = 0;
-        for (; t + 3 <= ntiles; t += 3) {
-            step(t, I0{});
-            step(t + 1, I1{});
-            step(t + 2, I2{});
-        }
-        if (t < ntiles) step(t, I0{});
-        if (t + 1 < ntiles) step(t + 1, I1{});
-        softmax_pv(s_lag, ntiles - 1, stage_at((ntiles - 1) % NSTAGE));
+        if (i < ntiles) step(i, I1{}, std::false_type{});
+        if (i + 1 < ntiles) step(i + 1, I2{}, std::false_type{});
+        if (i + 2 < ntiles) step(i + 2, I3{}, std::false_type{});
+        pv(pp0, pp1, stage_at((ntiles - 1) % NSTAGE));
     }
     __syncthreads();   // the merge below reuses the stage memory
 
