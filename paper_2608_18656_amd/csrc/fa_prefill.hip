@@ -43,7 +43,6 @@ constexpr int WR = 32;        // query rows per slot
 constexpr int NSLOT = 4;      // slots per workgroup
 constexpr int NT = 128 * NSLOT;   // threads per workgroup (two waves per slot)
 constexpr float kMaxLaneSum = 4096.0f;   // largest 16-weight lane sum kept without a rescale
-constexpr int NSTAGE = 4;     // LDS tile stages
 
 struct PrefillArgs {
     const void *q, *k, *v;
@@ -57,7 +56,7 @@ struct PrefillArgs {
     int nhg;          // head groups per key/value head (G / HW)
 };
 
-template <int D> struct Smem {
+template <int D, int NSTAGE> struct Smem {
     static constexpr int KS = D + 8;     // K row stride in 16-bit elements
     static constexpr int VTS = BC + 8;   // V^T row stride: 64 key positions + pad
     static constexpr int KSZ = BC * KS;
@@ -70,11 +69,17 @@ template <int D> struct Smem {
 // The first half of the workgroup stages K, the second half V.
 __device__ __forceinline__ bool kgroup_of(int tid) { return tid < NT / 2; }
 
+// Serial steps at D = 64: registers fit four waves per SIMD (two workgroups
+// per CU); at D = 128 the pipelined loop with two waves per SIMD.
+template <int D> constexpr bool kSerial = D == 64;
+
 template <typename TIN, typename TOUT, int D, bool CAUSAL>
-__global__ __launch_bounds__(NT, 1) void prefill_kernel(PrefillArgs a) {
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kSerial<D> ? 4 : 1, kSerial<D> ? 4 : 2))) void prefill_kernel(PrefillArgs a) {
     using S = typename TIN::scalar;
     using V8 = typename TIN::vec8;
-    using SM = Smem<D>;
+    constexpr bool SERIAL = kSerial<D>;
+    constexpr int NSTAGE = SERIAL ? 2 : 4;   // LDS tile stages
+    using SM = Smem<D, NSTAGE>;
     constexpr int KSTEPS = D / 16;          // QK^T contraction steps
     constexpr int DT = D / 32;              // output column tiles
     constexpr int LOADS = BC * D / 8 / NT;  // 16-byte chunks per thread per K (or V) tile
@@ -153,7 +158,8 @@ __global__ __launch_bounds__(NT, 1) void prefill_kernel(PrefillArgs a) {
     for (int i = 0; i < SL; ++i) goff[i] = (unsigned)(lkey(i) * row_elems + lcol(i));
     // Staging registers: NSET sets, so that a tile's global loads can be in
     // flight for NSET steps before it is written to LDS.
-    constexpr int NSET = D == 64 ? 2 : 1;
+    constexpr int NSET = SERIAL ? 1 : (D == 64 ? 4 : 2);
+    constexpr int ST_POS = 2;   // where a step writes its staged tile to LDS
     uint4_t sr[NSET][SL];
     auto gload = [&](int kb, int set) {   // tile starting at key kb (kb = 0, 64, 128, ...)
         if (kb + BC <= Nk) {
@@ -211,30 +217,39 @@ __global__ __launch_bounds__(NT, 1) void prefill_kernel(PrefillArgs a) {
     const int v_lane = SM::KSZ + lq * SM::VTS + 32 * kh + 8 * lh;
     auto stage_at = [&](int r) { return smem + r * SM::STAGE; };
 
-    // S^T = K Q^T for this wave's 32 keys of the tile held in `stage`
-    auto scores = [&](const unsigned short *stage) {
-        V8 ka[KSTEPS];
+    // K operands of this wave's 32 keys of the tile held in `stage`
+    auto kread = [&](const unsigned short *stage, V8 (&ka)[KSTEPS]) {
 #pragma unroll
         for (int kk = 0; kk < KSTEPS; ++kk)
             ka[kk] = as_vec8<V8>(*reinterpret_cast<const uint4_t *>(stage + k_lane + 16 * kk));
+    };
+    // S^T = K Q^T
+    auto qk = [&](const V8 (&ka)[KSTEPS]) {
         float16_t s = float16_t{};
 #pragma unroll
         for (int kk = 0; kk < KSTEPS; ++kk) s = mfma32(ka[kk], qf[kk], s);
         return s;
     };
+    auto scores = [&](const unsigned short *stage) {
+        V8 ka[KSTEPS];
+        kread(stage, ka);
+        return qk(ka);
+    };
 
+    // V^T operands of one tile for this wave (k-step order: dt, j)
+    auto vread = [&](const unsigned short *stage, half8_t (&va)[KSTEPS]) {
+#pragma unroll
+        for (int kk = 0; kk < KSTEPS; ++kk)
+            va[kk] = as_vec8<half8_t>(*reinterpret_cast<const uint4_t *>(
+                stage + v_lane + 32 * (kk >> 1) * SM::VTS + 16 * (kk & 1)));
+    };
     // O^T += V^T P^T with the weights of one tile (k-step j = keys 16 j .. 16 j
-    // + 15 of the wave's half), V^T read from `stage`
-    auto pv = [&](const half8_t &p0, const half8_t &p1, const unsigned short *stage) {
+    // + 15 of the wave's half)
+    auto pv = [&](const half8_t &p0, const half8_t &p1, const half8_t (&va)[KSTEPS]) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
-            half8_t va[2];
-#pragma unroll
-            for (int j = 0; j < 2; ++j)
-                va[j] = as_vec8<half8_t>(*reinterpret_cast<const uint4_t *>(
-                    stage + v_lane + 32 * dt * SM::VTS + 16 * j));
-            oacc[dt] = mfma32(va[0], p0, oacc[dt]);
-            oacc[dt] = mfma32(va[1], p1, oacc[dt]);
+            oacc[dt] = mfma32(va[2 * dt], p0, oacc[dt]);
+            oacc[dt] = mfma32(va[2 * dt + 1], p1, oacc[dt]);
         }
     };
 
@@ -292,68 +307,112 @@ __global__ __launch_bounds__(NT, 1) void prefill_kernel(PrefillArgs a) {
         l_run += ls;
     };
 
-    half8_t pp0, pp1;   // weights of the previous tile
-
-    // Tile loop, software-pipelined inside each wave: step i computes the
-    // scores of tile i + 1 and the PV product of tile i - 1 on the matrix
-    // cores while the softmax of tile i runs on the vector ALU; the three
-    // streams are independent, so the scheduler interleaves them.  Tile j sits
-    // in LDS stage j % 4 from step j - 2 (written from registers loaded in that
-    // step, or at D = 64 in the step before) until its V is read in step j + 1.
-    if (ntiles > 0) {
-        gload(0, 0);
-        sstore(stage_at(0), 0);
-    }
-    if (ntiles > 1) {
-        gload(BC, 1 % NSET);
-        sstore(stage_at(1), 1 % NSET);
-    }
-    if (NSET == 2 && ntiles > 2) gload(2 * BC, 0);
-    __syncthreads();
-    float16_t s_cur = scores(stage_at(0));
-    auto step = [&](int i, auto R, auto FIRST) {
-        constexpr int r = decltype(R)::value;
-        constexpr bool first = decltype(FIRST)::value;
-        const bool more = i + 2 < ntiles;
-        if (NSET == 2) {
-            if (i + 3 < ntiles) gload((i + 3) * BC, (r + 1) % 2);
-        } else if (more) {
-            gload((i + 2) * BC, 0);
+    if constexpr (SERIAL) {
+        // One tile per step, in order: scores, softmax, PV; the loads of the
+        // next tile are in flight meanwhile and it is written to the other
+        // LDS stage at the end of the step.  Latency is hidden by the other
+        // waves on the SIMD (two workgroups per CU).
+        if (ntiles > 0) {
+            gload(0, 0);
+            sstore(stage_at(0), 0);
         }
-        mask(s_cur, i);
-        // independent work of the step: scores of tile i + 1 and PV of tile
-        // i - 1 on the matrix cores, softmax of tile i on the vector ALU
-        const float16_t s_next = scores(stage_at((r + 1) % NSTAGE));   // unused after the last tile
-        if constexpr (!first) pv(pp0, pp1, stage_at((r + NSTAGE - 1) % NSTAGE));
-        half8_t p0, p1;
-        exp_pack(s_cur, fresh ? 0.f : -m_run, p0, p1);
-        const float ls = sum_f16x16(p0, p1);
-        const bool bad = (!(ls <= kMaxLaneSum)) | fresh;
-        finish(s_cur, p0, p1, ls, bad);
-        pp0 = p0;
-        pp1 = p1;
-        s_cur = s_next;
-        if (more) sstore(stage_at((r + 2) % NSTAGE), r % NSET);
         __syncthreads();
-    };
-    using I0 = std::integral_constant<int, 0>;
-    using I1 = std::integral_constant<int, 1>;
-    using I2 = std::integral_constant<int, 2>;
-    using I3 = std::integral_constant<int, 3>;
-    if (ntiles > 0) {
-        step(0, I0{}, std::true_type{});
-        int i = 1;
-        // unrolled by four so that every stage offset is a constant
-        for (; i + 4 <= ntiles; i += 4) {
-            step(i, I1{}, std::false_type{});
-            step(i + 1, I2{}, std::false_type{});
-            step(i + 2, I3{}, std::false_type{});
-            step(i + 3, I0{}, std::false_type{});
+        auto sstep = [&](int i, auto R) {
+            constexpr int r = decltype(R)::value;
+            const bool more = i + 1 < ntiles;
+            if (more) gload((i + 1) * BC, 0);
+            float16_t s = scores(stage_at(r));
+            mask(s, i);
+            half8_t p0, p1;
+            exp_pack(s, fresh ? 0.f : -m_run, p0, p1);
+            const float ls = sum_f16x16(p0, p1);
+            finish(s, p0, p1, ls, (!(ls <= kMaxLaneSum)) | fresh);
+            half8_t va[KSTEPS];
+            vread(stage_at(r), va);
+            pv(p0, p1, va);
+            if (more) sstore(stage_at(r ^ 1), 0);
+            __syncthreads();
+        };
+        int i = 0;
+        for (; i + 2 <= ntiles; i += 2) {
+            sstep(i, std::integral_constant<int, 0>{});
+            sstep(i + 1, std::integral_constant<int, 1>{});
         }
-        if (i < ntiles) step(i, I1{}, std::false_type{});
-        if (i + 1 < ntiles) step(i + 1, I2{}, std::false_type{});
-        if (i + 2 < ntiles) step(i + 2, I3{}, std::false_type{});
-        pv(pp0, pp1, stage_at((ntiles - 1) % NSTAGE));
+        if (i < ntiles) sstep(i, std::integral_constant<int, 0>{});
+    } else {
+        half8_t pp0, pp1;   // weights of the previous tile
+        // At D = 64 the V^T operands of the previous tile are read at the end of
+        // the step before (their LDS latency then overlaps the barrier); at D = 128
+        // the registers are not there and they are read where they are used.
+        constexpr bool VPRE = D == 64;
+        half8_t vprev[KSTEPS];
+
+        // Tile loop, software-pipelined inside each wave: step i computes the
+        // scores of tile i + 1 and the PV product of tile i - 1 on the matrix
+        // cores while the softmax of tile i runs on the vector ALU; the three
+        // streams are independent, so the scheduler interleaves them.  Tile j sits
+        // in LDS stage j % 4 from step j - 2 (written from registers loaded in that
+        // step, or at D = 64 in the step before) until its V is read in step j + 1.
+        // tile j: loaded into register set j % NSET in step j - 1 - NSET (the
+        // first ones here), written to LDS stage j % 4 in step j - 2
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+            if (j < ntiles) {
+                gload(j * BC, j % NSET);
+                sstore(stage_at(j), j % NSET);
+            }
+#pragma unroll
+        for (int j = 2; j <= NSET; ++j)
+            if (j < ntiles) gload(j * BC, j % NSET);
+        __syncthreads();
+        float16_t s_cur = scores(stage_at(0));
+        auto step = [&](int i, auto R, auto FIRST) {
+            constexpr int r = decltype(R)::value;
+            constexpr bool first = decltype(FIRST)::value;
+            const bool more = i + 2 < ntiles;
+            if (i + NSET + 1 < ntiles) gload((i + NSET + 1) * BC, (r + 1) % NSET);
+            if (NSET > 1 && ST_POS == 1 && more) sstore(stage_at((r + 2) % NSTAGE), (r + 2) % NSET);
+            mask(s_cur, i);
+            // independent work of the step: scores of tile i + 1 and PV of tile
+            // i - 1 on the matrix cores, softmax of tile i on the vector ALU
+            const float16_t s_next = scores(stage_at((r + 1) % NSTAGE));   // unused after the last tile
+            if constexpr (!first) {
+                if constexpr (!VPRE) vread(stage_at((r + NSTAGE - 1) % NSTAGE), vprev);
+                pv(pp0, pp1, vprev);
+            }
+            half8_t p0, p1;
+            exp_pack(s_cur, fresh ? 0.f : -m_run, p0, p1);
+            const float ls = sum_f16x16(p0, p1);
+            const bool bad = (!(ls <= kMaxLaneSum)) | fresh;
+            if (NSET > 1 && ST_POS == 2 && more) sstore(stage_at((r + 2) % NSTAGE), (r + 2) % NSET);
+            finish(s_cur, p0, p1, ls, bad);
+            pp0 = p0;
+            pp1 = p1;
+            if constexpr (VPRE) vread(stage_at(r), vprev);   // V of tile i, for the next step
+            s_cur = s_next;
+            if ((NSET == 1 || ST_POS == 0) && more) sstore(stage_at((r + 2) % NSTAGE), (r + 2) % NSET);
+            __syncthreads();
+        };
+        using I0 = std::integral_constant<int, 0>;
+        using I1 = std::integral_constant<int, 1>;
+        using I2 = std::integral_constant<int, 2>;
+        using I3 = std::integral_constant<int, 3>;
+        if (ntiles > 0) {
+            step(0, I0{}, std::true_type{});
+            int i = 1;
+            // unrolled by four so that every stage offset is a constant
+            for (; i + 4 <= ntiles; i += 4) {
+                step(i, I1{}, std::false_type{});
+                step(i + 1, I2{}, std::false_type{});
+                step(i + 2, I3{}, std::false_type{});
+                step(i + 3, I0{}, std::false_type{});
+            }
+            if (i < ntiles) step(i, I1{}, std::false_type{});
+            if (i + 1 < ntiles) step(i + 1, I2{}, std::false_type{});
+            if (i + 2 < ntiles) step(i + 2, I3{}, std::false_type{});
+            if constexpr (!VPRE) vread(stage_at((ntiles - 1) % NSTAGE), vprev);
+            pv(pp0, pp1, vprev);
+        }
     }
     __syncthreads();   // the merge below reuses the stage memory
 
