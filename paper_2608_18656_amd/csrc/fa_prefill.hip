@@ -30,6 +30,7 @@
 // Masked scores are -inf and give exactly 0 (the exponent factor is kept
 // strictly positive, also for scale = 0).  Keys past the end are read from a
 // clamped row and masked.  Normalisation happens once, after the last tile.
+#include <atomic>
 #include <type_traits>
 
 #include "fa_common.h"
@@ -54,6 +55,7 @@ struct PrefillArgs {
     int HW;           // query heads per workgroup (1, 2 or 4)
     int nmb;          // row blocks of 32 * (4 / HW) rows
     int nhg;          // head groups per key/value head (G / HW)
+    int pair;         // 1: every workgroup is resident at once; order heavy/light pairs
 };
 
 template <int D, int NSTAGE> struct Smem {
@@ -95,7 +97,14 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kSerial<D> ?
     const int RB = NSLOT / a.HW;
     const int per_mb = a.B * a.Hkv * a.nhg;
     const int bid = blockIdx.x;
-    const int mb = a.nmb - 1 - bid / per_mb;    // latest rows (most keys) first
+    // Row block of this workgroup.  Latest rows (most keys) first, so that
+    // the short causal blocks fill the tail; when the whole grid is resident
+    // at once (two workgroups per CU), the first half of the grid takes the
+    // long blocks in decreasing and the second half the short ones in
+    // increasing length, so that the two workgroups sharing a CU carry about
+    // the same total work.
+    const int q_ = bid / per_mb, half_ = (a.nmb + 1) / 2;
+    const int mb = (!a.pair || q_ < half_) ? a.nmb - 1 - q_ : q_ - half_;
     int rest = bid % per_mb;
     const int hg = rest % a.nhg;
     rest /= a.nhg;
@@ -471,6 +480,17 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kSerial<D> ?
     }
 }
 
+// Compute units of the current device (cached per device; 0 if unknown).
+int cu_count() {
+    static std::atomic<int> cached[64] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+    int n = cached[dev].load(std::memory_order_relaxed);
+    if (n == 0 && hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess)
+        cached[dev].store(n, std::memory_order_relaxed);
+    return n;
+}
+
 template <typename TIN, typename TOUT, int D, bool CAUSAL>
 hipError_t launch_t(const Problem &p, hipStream_t stream) {
     PrefillArgs a;
@@ -485,9 +505,11 @@ hipError_t launch_t(const Problem &p, hipStream_t stream) {
     const int RB = NSLOT / a.HW;
     a.nmb = (p.Nq + WR * RB - 1) / (WR * RB);
     a.nhg = G / a.HW;
+    a.pair = 0;
     const long long nblocks = (long long)a.nmb * p.B * p.Hkv * a.nhg;
     if (nblocks <= 0) return hipSuccess;
     if (nblocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+    if (kSerial<D> && p.causal) a.pair = nblocks <= 2LL * cu_count() ? 1 : 0;
     hipLaunchKernelGGL((prefill_kernel<TIN, TOUT, D, CAUSAL>), dim3((unsigned)nblocks), dim3(NT),
                        0, stream, a);
     return hipGetLastError();
