@@ -220,6 +220,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kSerial<D> ?
     for (int dt = 0; dt < DT; ++dt) oacc[dt] = float16_t{};
     float m_run = -INFINITY;   // exponent base (log2 domain), same in lanes l and l^32
     float l_run = 0.f;         // this lane's part of the row sum
+    float nbase = 0.f;         // -m_run, or 0 while the row has no base
     bool fresh = true;         // some row of the wave has no base yet (wave-uniform)
 
     const int k_lane = (32 * kh + lq) * SM::KS + 8 * lh;
@@ -285,15 +286,30 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kSerial<D> ?
         p1 = pack_f16x8(p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]);
     };
 
+    // row sum += the 16 f16 weights of the lane, in fp32 (dot products with (1, 1))
+    auto add_sum = [&](float l, const half8_t &p0, const half8_t &p1) {
+        const half2_t one = {(_Float16)1.0f, (_Float16)1.0f};
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            l = __builtin_amdgcn_fdot2(half2_t{p0[2 * i], p0[2 * i + 1]}, one, l, false);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            l = __builtin_amdgcn_fdot2(half2_t{p1[2 * i], p1[2 * i + 1]}, one, l, false);
+        return l;
+    };
     // Online softmax of one tile.  The weights are first formed against the
-    // current base and kept if each lane's sum of its 16 weights stays at most
-    // 4096 (every weight then fits f16 with room to spare and no rescale is
+    // current base and kept if the lane's 16 weights add at most 4096 to its
+    // row sum (every weight then fits f16 with room to spare and no rescale is
     // due; the row maximum is never formed).  Only when some row outgrows its
     // base that far (or a row has no base yet) is the row maximum taken, the
     // accumulator and row sum rescaled to it and the weights recomputed.  The
     // row sum adds, in fp32, the f16 weights that also feed the matrix product.
-    auto finish = [&](const float16_t &s, half8_t &p0, half8_t &p1, float ls, bool bad) {
-        if (__builtin_amdgcn_ballot_w64(bad) != 0) {
+    auto softmax = [&](const float16_t &s, half8_t &p0, half8_t &p1) {
+        exp_pack(s, nbase, p0, p1);
+        const float l_old = l_run;
+        l_run = add_sum(l_run, p0, p1);
+        const bool over = !(l_run <= l_old + kMaxLaneSum);
+        if (fresh || __builtin_amdgcn_ballot_w64(over) != 0) {
             float mx = max3(s[0], s[1], s[2]);
             mx = max3(mx, s[3], s[4]);
             mx = max3(mx, s[5], s[6]);
@@ -306,14 +322,13 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kSerial<D> ?
             const float m_new = __builtin_fmaxf(m_run, mx * a.c);
             const float alpha = (m_new == -INFINITY) ? 1.f : exp2_fast(m_run - m_new);
             m_run = m_new;
-            l_run *= alpha;
+            nbase = (m_new == -INFINITY) ? 0.f : -m_new;
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
-            exp_pack(s, (m_run == -INFINITY) ? 0.f : -m_run, p0, p1);
-            ls = sum_f16x16(p0, p1);
+            exp_pack(s, nbase, p0, p1);
+            l_run = add_sum(l_old * alpha, p0, p1);
             fresh = __builtin_amdgcn_ballot_w64(m_run == -INFINITY) != 0;
         }
-        l_run += ls;
     };
 
     if constexpr (SERIAL) {
@@ -333,9 +348,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kSerial<D> ?
             float16_t s = scores(stage_at(r));
             mask(s, i);
             half8_t p0, p1;
-            exp_pack(s, fresh ? 0.f : -m_run, p0, p1);
-            const float ls = sum_f16x16(p0, p1);
-            finish(s, p0, p1, ls, (!(ls <= kMaxLaneSum)) | fresh);
+            softmax(s, p0, p1);
             half8_t va[KSTEPS];
             vread(stage_at(r), va);
             pv(p0, p1, va);
@@ -390,11 +403,8 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kSerial<D> ?
                 pv(pp0, pp1, vprev);
             }
             half8_t p0, p1;
-            exp_pack(s_cur, fresh ? 0.f : -m_run, p0, p1);
-            const float ls = sum_f16x16(p0, p1);
-            const bool bad = (!(ls <= kMaxLaneSum)) | fresh;
+            softmax(s_cur, p0, p1);
             if (NSET > 1 && ST_POS == 2 && more) sstore(stage_at((r + 2) % NSTAGE), (r + 2) % NSET);
-            finish(s_cur, p0, p1, ls, bad);
             pp0 = p0;
             pp1 = p1;
             if constexpr (VPRE) vread(stage_at(r), vprev);   // V of tile i, for the next step
