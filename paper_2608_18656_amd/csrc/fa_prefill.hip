@@ -15,18 +15,24 @@
 // the per-key recurrence of Alg. 1):
 //   S^T = K Q^T        32x32x16 MFMA; A = 32 K rows from LDS, B = the wave's
 //                      32 query rows, kept in registers for the whole kernel
-//   row max / exp2     scores stay in the MFMA result registers; lane l owns
-//                      query row l%32, so the row max needs one exchange with
-//                      lane l^32; scale and log2(e) fold into one multiply-add
+//   softmax            scores stay in the MFMA result registers; lane l owns
+//                      query row l%32 (a row maximum needs one exchange with
+//                      lane l^32); scale and log2(e) fold into one
+//                      multiply-add ahead of exp2; weights packed to fp16
 //   O^T += V^T P^T     32x32x16 fp16 MFMA; P straight from the score registers,
 //                      V^T operands read from a transposed copy of the V tile
 //                      that the staging step writes into LDS (a transposing
-//                      LDS read runs at about a third of the plain 16-byte
-//                      read rate on gfx950, so the transpose is paid once per
-//                      tile in the copy instead of once per wave)
-// The exponent base is raised only when a row's maximum grows by more than
-// 2^8 (log2 domain), so the accumulator rescale is skipped on most tiles; sum
-// and accumulator always share the base, so the result is unchanged.
+//                      LDS read is slower than the plain 16-byte read on
+//                      gfx950, so the transpose is paid once per tile in the
+//                      copy instead of once per wave)
+// The exponent base only moves when a tile's weights against the current base
+// grow too large (see the softmax step below), so the accumulator rescale is
+// skipped on most tiles; sum and accumulator always share the base, so the
+// result is unchanged.
+// At D = 64 the steps of a wave run in order and the kernel fits 128 VGPRs,
+// so two workgroups share a CU (four waves per SIMD) and hide each other's
+// latencies; at D = 128 one workgroup per CU software-pipelines each wave's
+// steps instead.
 // Masked scores are -inf and give exactly 0 (the exponent factor is kept
 // strictly positive, also for scale = 0).  Keys past the end are read from a
 // clamped row and masked.  Normalisation happens once, after the last tile.
