@@ -1,15 +1,15 @@
 // fa_prefill.hip -- prefill attention forward on gfx950 matrix cores.
 //
-// Work split.  A workgroup has 8 waves and owns four (query head, 32-row
-// block) slots that read the same key/value head.  When the group size
-// G = Hq/Hkv allows, the four slots are four query heads of one key/value
-// group at the same rows -- the GPU form of the inter-head packing of
-// Sec. 4.1.1 and the GQA reuse of Sec. 4.1.2 (iv): every K/V tile staged in
-// LDS serves four heads, and all slots share one causal extent.  Otherwise
-// (G = 1 or odd) the slots are consecutive row blocks of one head.  Each slot
-// has two waves; keys are streamed in tiles of 64 and wave kh of a slot takes
-// keys 32 kh .. 32 kh + 31 of every tile, so the sequential chain per wave is
-// half the tile work.  The two waves' states are merged through LDS at the end.
+// Work split.  A workgroup owns four (query head, 32-row block) slots that
+// read the same key/value head.  When the group size G = Hq/Hkv allows, the
+// four slots are four query heads of one key/value group at the same rows --
+// the GPU form of the inter-head packing of Sec. 4.1.1 and the GQA reuse of
+// Sec. 4.1.2 (iv): every K/V tile staged in LDS serves four heads, and all
+// slots share one causal extent.  Otherwise (G = 1 or odd) the slots are
+// consecutive row blocks of one head.  Every wave handles 32 rows and 32 keys
+// of each tile.  At D = 64 a slot has two waves (64-key tiles; wave kh takes
+// keys 32 kh .. 32 kh + 31) whose states are merged through LDS at the end; at
+// D = 128 one wave (32-key tiles).
 //
 // Per wave and tile, the blocked streaming softmax (Alg. 2 state carry over
 // the per-key recurrence of Alg. 1):
@@ -29,10 +29,9 @@
 // grow too large (see the softmax step below), so the accumulator rescale is
 // skipped on most tiles; sum and accumulator always share the base, so the
 // result is unchanged.
-// At D = 64 the steps of a wave run in order and the kernel fits 128 VGPRs,
-// so two workgroups share a CU (four waves per SIMD) and hide each other's
-// latencies; at D = 128 one workgroup per CU software-pipelines each wave's
-// steps instead.
+// A wave's steps run in order; latency is hidden by running several
+// workgroups per CU (two: four waves per SIMD at D = 64 within 128 VGPRs; two
+// 4-wave workgroups at D = 128), whose barriers are independent.
 // Masked scores are -inf and give exactly 0 (the exponent factor is kept
 // strictly positive, also for scale = 0).  Keys past the end are read from a
 // clamped row and masked.  Normalisation happens once, after the last tile.
@@ -45,10 +44,8 @@
 namespace fa {
 namespace {
 
-constexpr int BC = 64;        // keys per tile (two halves of 32, one per wave)
 constexpr int WR = 32;        // query rows per slot
 constexpr int NSLOT = 4;      // slots per workgroup
-constexpr int NT = 128 * NSLOT;   // threads per workgroup (two waves per slot)
 constexpr float kMaxLaneSum = 4096.0f;   // largest 16-weight lane sum kept without a rescale
 
 struct PrefillArgs {
@@ -64,33 +61,36 @@ struct PrefillArgs {
     int pair;         // 1: every workgroup is resident at once; order heavy/light pairs
 };
 
-template <int D, int NSTAGE> struct Smem {
-    static constexpr int KS = D + 8;     // K row stride in 16-bit elements
-    static constexpr int VTS = BC + 8;   // V^T row stride: 64 key positions + pad
+// Tile shape per head size.  Every wave handles 32 query rows and 32 keys of
+// a tile.  D = 64: two waves per slot (64-key tiles, key halves merged at the
+// end), 8-wave workgroups of at most 128 VGPRs, two per CU (four waves per
+// SIMD).  D = 128: the accumulator (64 VGPRs) and Q (32) leave no room for
+// that, so one wave per slot (32-key tiles) and 4-wave workgroups, two per CU
+// (two waves per SIMD, from independent workgroups).  Two LDS stages in both.
+template <int D> struct Cfg {
+    static constexpr int NQ = D == 64 ? 2 : 1;       // waves per slot
+    static constexpr int WPE = D == 64 ? 4 : 2;      // waves per SIMD
+    static constexpr int WPC = D == 64 ? 2 : 2;      // workgroups per CU
+    static constexpr int BC = 32 * NQ;               // keys per tile
+    static constexpr int NT = 64 * NSLOT * NQ;       // threads per workgroup
+    static constexpr int NSTAGE = 2;                 // LDS tile stages
+    static constexpr int KS = D + 8;                 // K row stride in 16-bit elements
+    static constexpr int VTS = BC + 8;               // V^T row stride: BC key positions + pad
     static constexpr int KSZ = BC * KS;
     static constexpr int VSZ = D * VTS;
     static constexpr int STAGE = KSZ + VSZ;
-    static constexpr int MERGE = NSLOT * ((D / 32) * 16 + 2) * 64;   // floats
+    static constexpr int MERGE = NQ > 1 ? NSLOT * (NQ / 2) * ((D / 32) * 16 + 2) * 64 : 0;  // floats
     static constexpr int WORDS = (NSTAGE * STAGE) > (2 * MERGE) ? NSTAGE * STAGE : 2 * MERGE;
 };
 
-// The first half of the workgroup stages K, the second half V.
-__device__ __forceinline__ bool kgroup_of(int tid) { return tid < NT / 2; }
-
-// Serial steps at D = 64: registers fit four waves per SIMD (two workgroups
-// per CU); at D = 128 the pipelined loop with two waves per SIMD.
-template <int D> constexpr bool kSerial = D == 64;
-
 template <typename TIN, typename TOUT, int D, bool CAUSAL>
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kSerial<D> ? 4 : 1, kSerial<D> ? 4 : 2))) void prefill_kernel(PrefillArgs a) {
+__global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<D>::WPE, Cfg<D>::WPE))) void prefill_kernel(PrefillArgs a) {
     using S = typename TIN::scalar;
     using V8 = typename TIN::vec8;
-    constexpr bool SERIAL = kSerial<D>;
-    constexpr int NSTAGE = SERIAL ? 2 : 4;   // LDS tile stages
-    using SM = Smem<D, NSTAGE>;
+    using SM = Cfg<D>;
+    constexpr int NQ = SM::NQ, BC = SM::BC, NT = SM::NT, NSTAGE = SM::NSTAGE;
     constexpr int KSTEPS = D / 16;          // QK^T contraction steps
     constexpr int DT = D / 32;              // output column tiles
-    constexpr int LOADS = BC * D / 8 / NT;  // 16-byte chunks per thread per K (or V) tile
     constexpr int CPR = D / 8;              // 16-byte chunks per row
     constexpr bool IN_BF16 = __is_same(TIN, bf16_t);
 
@@ -99,7 +99,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kSerial<D> ?
     const int tid = threadIdx.x;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int l = tid & 63, lq = l & 31, lh = l >> 5;
-    const int kh = w / NSLOT, slot = w % NSLOT;
+    const int kh = w / NSLOT, slot = w % NSLOT;   // kh: the wave's 32 keys of a tile
     const int RB = NSLOT / a.HW;
     const int per_mb = a.B * a.Hkv * a.nhg;
     const int bid = blockIdx.x;
@@ -146,45 +146,42 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kSerial<D> ?
         }
     }
 
-    // Tile staging.  Waves 0-3 copy K rows (chunk c = tid + 256 i: key c / CPR,
-    // 16-byte column chunk c % CPR).  Waves 4-7 stage V transposed: unit u
-    // holds keys 2p, 2p+1 (p = u % 32) of column chunk u / 32 and writes eight
-    // 32-bit words, each the (2p, 2p+1) pair of one column d, into row d of V^T
-    // (as fp16).  Within every 16 keys the V^T positions swap bits 2 and 3 of
+    // Tile staging.  The first half of the workgroup copies K rows (chunk
+    // c = st + (NT / 2) i: key c / CPR, 16-byte column chunk c % CPR); the second
+    // half stages V transposed: unit u holds keys 2p, 2p+1 (p = u % KP) of
+    // column chunk u / KP and writes eight 32-bit words, each the (2p, 2p+1)
+    // pair of one column d, into row d of V^T (as fp16).  Within every 16 keys the V^T positions swap bits 2 and 3 of
     // the key index, so that the eight keys one MFMA lane needs are contiguous.
     // Global addresses advance by one tile per step; only a tile that reaches
     // past the last key recomputes them with the row index clamped (those keys
     // are masked).
-    constexpr int SL = 16 * D / NT;             // 16-byte loads per thread per tile
-    const S *kvbase = reinterpret_cast<const S *>(kgroup_of(tid) ? a.k : a.v) +
+    constexpr int SL = BC * D / (4 * NT);       // 16-byte loads per thread per tile
+    constexpr int KP = BC / 2;                  // key pairs per tile
+    const bool kgroup = tid < NT / 2;           // first half of the workgroup: K
+    const S *kvbase = reinterpret_cast<const S *>(kgroup ? a.k : a.v) +
                       ((size_t)b * Nk * a.Hkv + g) * D;
-    const bool kgroup = kgroup_of(tid);
     const int st = kgroup ? tid : tid - NT / 2;
     const size_t row_elems = (size_t)a.Hkv * D;      // elements between consecutive keys
     // tile-relative key and column of load i of this thread
     auto lkey = [&](int i) {
-        return kgroup ? (st + (NT / 2) * i) / CPR : 2 * ((st + (NT / 2) * (i >> 1)) % 32) + (i & 1);
+        return kgroup ? (st + (NT / 2) * i) / CPR : 2 * ((st + (NT / 2) * (i >> 1)) % KP) + (i & 1);
     };
     auto lcol = [&](int i) {
-        return kgroup ? 8 * ((st + (NT / 2) * i) % CPR) : 8 * ((st + (NT / 2) * (i >> 1)) / 32);
+        return kgroup ? 8 * ((st + (NT / 2) * i) % CPR) : 8 * ((st + (NT / 2) * (i >> 1)) / KP);
     };
     unsigned goff[SL];                               // tile-relative element offsets
 #pragma unroll
     for (int i = 0; i < SL; ++i) goff[i] = (unsigned)(lkey(i) * row_elems + lcol(i));
-    // Staging registers: NSET sets, so that a tile's global loads can be in
-    // flight for NSET steps before it is written to LDS.
-    constexpr int NSET = SERIAL ? 1 : (D == 64 ? 4 : 2);
-    constexpr int ST_POS = 2;   // where a step writes its staged tile to LDS
-    uint4_t sr[NSET][SL];
-    auto gload = [&](int kb, int set) {   // tile starting at key kb (kb = 0, 64, 128, ...)
+    uint4_t sr[SL];   // the next tile, in flight during a step
+    auto gload = [&](int kb) {   // tile starting at key kb (a multiple of BC)
         if (kb + BC <= Nk) {
             const S *tb = kvbase + (size_t)kb * row_elems;
 #pragma unroll
-            for (int i = 0; i < SL; ++i) sr[set][i] = ld16(tb + goff[i]);
+            for (int i = 0; i < SL; ++i) sr[i] = ld16(tb + goff[i]);
         } else {
 #pragma unroll
             for (int i = 0; i < SL; ++i)
-                sr[set][i] = ld16(kvbase + (size_t)min(kb + lkey(i), Nk - 1) * row_elems + lcol(i));
+                sr[i] = ld16(kvbase + (size_t)min(kb + lkey(i), Nk - 1) * row_elems + lcol(i));
         }
     };
     // LDS destination (element offset inside a stage) of load i
@@ -194,15 +191,15 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kSerial<D> ?
         const int pos = (key & ~12) | ((key & 4) << 1) | ((key & 8) >> 1);
         return SM::KSZ + lcol(i) * SM::VTS + pos;   // row d = lcol + e, position pos
     };
-    auto sstore = [&](unsigned short *stage, int set) {
+    auto sstore = [&](unsigned short *stage) {
         if (kgroup) {
 #pragma unroll
-            for (int i = 0; i < SL; ++i) st16(stage + sdst(i), sr[set][i]);
+            for (int i = 0; i < SL; ++i) st16(stage + sdst(i), sr[i]);
         } else {
 #pragma unroll
             for (int u = 0; u < SL / 2; ++u) {
                 unsigned *vt = reinterpret_cast<unsigned *>(stage + sdst(2 * u));
-                const uint4_t x = sr[set][2 * u], y = sr[set][2 * u + 1];
+                const uint4_t x = sr[2 * u], y = sr[2 * u + 1];
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
                     const unsigned xe = x[e >> 1], ye = y[e >> 1];
@@ -337,115 +334,43 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kSerial<D> ?
         }
     };
 
-    if constexpr (SERIAL) {
-        // One tile per step, in order: scores, softmax, PV; the loads of the
-        // next tile are in flight meanwhile and it is written to the other
-        // LDS stage at the end of the step.  Latency is hidden by the other
-        // waves on the SIMD (two workgroups per CU).
-        if (ntiles > 0) {
-            gload(0, 0);
-            sstore(stage_at(0), 0);
-        }
-        __syncthreads();
-        auto sstep = [&](int i, auto R) {
-            constexpr int r = decltype(R)::value;
-            const bool more = i + 1 < ntiles;
-            if (more) gload((i + 1) * BC, 0);
-            float16_t s = scores(stage_at(r));
-            mask(s, i);
-            half8_t p0, p1;
-            softmax(s, p0, p1);
-            half8_t va[KSTEPS];
-            vread(stage_at(r), va);
-            pv(p0, p1, va);
-            if (more) sstore(stage_at(r ^ 1), 0);
-            __syncthreads();
-        };
-        int i = 0;
-        for (; i + 2 <= ntiles; i += 2) {
-            sstep(i, std::integral_constant<int, 0>{});
-            sstep(i + 1, std::integral_constant<int, 1>{});
-        }
-        if (i < ntiles) sstep(i, std::integral_constant<int, 0>{});
-    } else {
-        half8_t pp0, pp1;   // weights of the previous tile
-        // At D = 64 the V^T operands of the previous tile are read at the end of
-        // the step before (their LDS latency then overlaps the barrier); at D = 128
-        // the registers are not there and they are read where they are used.
-        constexpr bool VPRE = D == 64;
-        half8_t vprev[KSTEPS];
-
-        // Tile loop, software-pipelined inside each wave: step i computes the
-        // scores of tile i + 1 and the PV product of tile i - 1 on the matrix
-        // cores while the softmax of tile i runs on the vector ALU; the three
-        // streams are independent, so the scheduler interleaves them.  Tile j sits
-        // in LDS stage j % 4 from step j - 2 (written from registers loaded in that
-        // step, or at D = 64 in the step before) until its V is read in step j + 1.
-        // tile j: loaded into register set j % NSET in step j - 1 - NSET (the
-        // first ones here), written to LDS stage j % 4 in step j - 2
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-            if (j < ntiles) {
-                gload(j * BC, j % NSET);
-                sstore(stage_at(j), j % NSET);
-            }
-#pragma unroll
-        for (int j = 2; j <= NSET; ++j)
-            if (j < ntiles) gload(j * BC, j % NSET);
-        __syncthreads();
-        float16_t s_cur = scores(stage_at(0));
-        auto step = [&](int i, auto R, auto FIRST) {
-            constexpr int r = decltype(R)::value;
-            constexpr bool first = decltype(FIRST)::value;
-            const bool more = i + 2 < ntiles;
-            if (i + NSET + 1 < ntiles) gload((i + NSET + 1) * BC, (r + 1) % NSET);
-            if (NSET > 1 && ST_POS == 1 && more) sstore(stage_at((r + 2) % NSTAGE), (r + 2) % NSET);
-            mask(s_cur, i);
-            // independent work of the step: scores of tile i + 1 and PV of tile
-            // i - 1 on the matrix cores, softmax of tile i on the vector ALU
-            const float16_t s_next = scores(stage_at((r + 1) % NSTAGE));   // unused after the last tile
-            if constexpr (!first) {
-                if constexpr (!VPRE) vread(stage_at((r + NSTAGE - 1) % NSTAGE), vprev);
-                pv(pp0, pp1, vprev);
-            }
-            half8_t p0, p1;
-            softmax(s_cur, p0, p1);
-            if (NSET > 1 && ST_POS == 2 && more) sstore(stage_at((r + 2) % NSTAGE), (r + 2) % NSET);
-            pp0 = p0;
-            pp1 = p1;
-            if constexpr (VPRE) vread(stage_at(r), vprev);   // V of tile i, for the next step
-            s_cur = s_next;
-            if ((NSET == 1 || ST_POS == 0) && more) sstore(stage_at((r + 2) % NSTAGE), (r + 2) % NSET);
-            __syncthreads();
-        };
-        using I0 = std::integral_constant<int, 0>;
-        using I1 = std::integral_constant<int, 1>;
-        using I2 = std::integral_constant<int, 2>;
-        using I3 = std::integral_constant<int, 3>;
-        if (ntiles > 0) {
-            step(0, I0{}, std::true_type{});
-            int i = 1;
-            // unrolled by four so that every stage offset is a constant
-            for (; i + 4 <= ntiles; i += 4) {
-                step(i, I1{}, std::false_type{});
-                step(i + 1, I2{}, std::false_type{});
-                step(i + 2, I3{}, std::false_type{});
-                step(i + 3, I0{}, std::false_type{});
-            }
-            if (i < ntiles) step(i, I1{}, std::false_type{});
-            if (i + 1 < ntiles) step(i + 1, I2{}, std::false_type{});
-            if (i + 2 < ntiles) step(i + 2, I3{}, std::false_type{});
-            if constexpr (!VPRE) vread(stage_at((ntiles - 1) % NSTAGE), vprev);
-            pv(pp0, pp1, vprev);
-        }
+    // Tile loop: one tile per step, in order -- scores, softmax, PV.  The next
+    // tile's global loads are in flight during the step, and it is written
+    // to the other LDS stage at the end of the step.  The latencies of a
+    // step are hidden by the waves of the other workgroups on the CU, whose
+    // barriers are independent of this one's.
+    if (ntiles > 0) {
+        gload(0);
+        sstore(stage_at(0));
     }
+    __syncthreads();
+    auto step = [&](int i, auto R) {   // R: stage of tile i (i % 2)
+        constexpr int r = decltype(R)::value;
+        const bool more = i + 1 < ntiles;
+        if (more) gload((i + 1) * BC);
+        float16_t s = scores(stage_at(r));
+        mask(s, i);
+        half8_t p0, p1;
+        softmax(s, p0, p1);
+        half8_t va[KSTEPS];
+        vread(stage_at(r), va);
+        pv(p0, p1, va);
+        if (more) sstore(stage_at(r ^ 1));
+        __syncthreads();
+    };
+    int i = 0;
+    for (; i + 2 <= ntiles; i += 2) {   // unrolled by two: stage offsets are constants
+        step(i, std::integral_constant<int, 0>{});
+        step(i + 1, std::integral_constant<int, 1>{});
+    }
+    if (i < ntiles) step(i, std::integral_constant<int, 0>{});
     __syncthreads();   // the merge below reuses the stage memory
 
     // ---- merge the two key halves of each slot through LDS
     float *mf = reinterpret_cast<float *>(smem);
     constexpr int NV = DT * 16 + 2;
     float *mine = mf + (slot * NV) * 64 + l;
-    if (kh == 1) {
+    if (NQ == 2 && kh == 1) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -453,9 +378,9 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kSerial<D> ?
         mine[(DT * 16) * 64] = m_run;
         mine[(DT * 16 + 1) * 64] = l_run;
     }
-    __syncthreads();
-    if (kh == 1 || !live) return;
-    {
+    if (NQ == 2) __syncthreads();
+    if (kh != 0 || !live) return;
+    if (NQ == 2) {
         const float m1 = mine[(DT * 16) * 64];
         const float l1 = mine[(DT * 16 + 1) * 64];
         const float M = __builtin_fmaxf(m_run, m1);
@@ -525,8 +450,8 @@ hipError_t launch_t(const Problem &p, hipStream_t stream) {
     const long long nblocks = (long long)a.nmb * p.B * p.Hkv * a.nhg;
     if (nblocks <= 0) return hipSuccess;
     if (nblocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-    if (kSerial<D> && p.causal) a.pair = nblocks <= 2LL * cu_count() ? 1 : 0;
-    hipLaunchKernelGGL((prefill_kernel<TIN, TOUT, D, CAUSAL>), dim3((unsigned)nblocks), dim3(NT),
+    if (p.causal) a.pair = nblocks <= (long long)Cfg<D>::WPC * cu_count() ? 1 : 0;
+    hipLaunchKernelGGL((prefill_kernel<TIN, TOUT, D, CAUSAL>), dim3((unsigned)nblocks), dim3(Cfg<D>::NT),
                        0, stream, a);
     return hipGetLastError();
 }
