@@ -33,8 +33,9 @@
 // workgroups per CU (two: four waves per SIMD at D = 64 within 128 VGPRs; two
 // 4-wave workgroups at D = 128), whose barriers are independent.
 // Masked scores are -inf and give exactly 0 (the exponent factor is kept
-// strictly positive, also for scale = 0).  Keys past the end are read from a
-// clamped row and masked.  Normalisation happens once, after the last tile.
+// strictly positive, also for scale = 0).  Keys past the end read as zero
+// (buffer loads with the tensor's extent as the range) and are masked.
+// Normalisation happens once, after the last tile.
 #include <atomic>
 #include <type_traits>
 
@@ -150,14 +151,14 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
     // c = st + (NT / 2) i: key c / CPR, 16-byte column chunk c % CPR); the second
     // half stages V transposed: unit u holds keys 2p, 2p+1 (p = u % KP) of
     // column chunk u / KP and writes eight 32-bit words, each the (2p, 2p+1)
-    // pair of one column d, into row d of V^T (as fp16).  Within every 16 keys the V^T positions swap bits 2 and 3 of
-    // the key index, so that the eight keys one MFMA lane needs are contiguous.
-    // Global addresses advance by one tile per step; only a tile that reaches
-    // past the last key recomputes them with the row index clamped (those keys
-    // are masked).
+    // pair of one column d, into row d of V^T (as fp16).  Within every 16 keys
+    // the V^T positions swap bits 2 and 3 of the key index, so that the eight
+    // keys one MFMA lane needs are contiguous.  Loads are buffer loads: the
+    // tile's first key row is the (scalar) base and each lane keeps a fixed
+    // byte offset, so a step spends no vector instructions on addresses.
     constexpr int SL = BC * D / (4 * NT);       // 16-byte loads per thread per tile
     constexpr int KP = BC / 2;                  // key pairs per tile
-    const bool kgroup = tid < NT / 2;           // first half of the workgroup: K
+    const bool kgroup = w < NT / 128;           // first half of the workgroup: K (wave-uniform)
     const S *kvbase = reinterpret_cast<const S *>(kgroup ? a.k : a.v) +
                       ((size_t)b * Nk * a.Hkv + g) * D;
     const int st = kgroup ? tid : tid - NT / 2;
@@ -169,20 +170,21 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
     auto lcol = [&](int i) {
         return kgroup ? 8 * ((st + (NT / 2) * i) % CPR) : 8 * ((st + (NT / 2) * (i >> 1)) / KP);
     };
-    unsigned goff[SL];                               // tile-relative element offsets
+    int goff[SL];                                    // tile-relative byte offsets
 #pragma unroll
-    for (int i = 0; i < SL; ++i) goff[i] = (unsigned)(lkey(i) * row_elems + lcol(i));
+    for (int i = 0; i < SL; ++i) goff[i] = (int)((lkey(i) * row_elems + lcol(i)) * sizeof(S));
     uint4_t sr[SL];   // the next tile, in flight during a step
     auto gload = [&](int kb) {   // tile starting at key kb (a multiple of BC)
-        if (kb + BC <= Nk) {
-            const S *tb = kvbase + (size_t)kb * row_elems;
+        // buffer view from the tile's first key to the end of the last key
+        // row: loads of keys past the end return zero (and are masked)
+        const S *tb = kvbase + (size_t)kb * row_elems;
+        const long long rem = ((long long)(Nk - 1 - kb) * (long long)row_elems + D) * (long long)sizeof(S);
+        const int nrec = (int)(rem < 0x7fffffffLL ? rem : 0x7fffffffLL);
+        const __amdgpu_buffer_rsrc_t rs =
+            __builtin_amdgcn_make_buffer_rsrc(const_cast<S *>(tb), (short)0, nrec, 0x00020000);
 #pragma unroll
-            for (int i = 0; i < SL; ++i) sr[i] = ld16(tb + goff[i]);
-        } else {
-#pragma unroll
-            for (int i = 0; i < SL; ++i)
-                sr[i] = ld16(kvbase + (size_t)min(kb + lkey(i), Nk - 1) * row_elems + lcol(i));
-        }
+        for (int i = 0; i < SL; ++i)
+            sr[i] = __builtin_bit_cast(uint4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, goff[i], 0, 0));
     };
     // LDS destination (element offset inside a stage) of load i
     auto sdst = [&](int i) {
@@ -236,11 +238,15 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
         for (int kk = 0; kk < KSTEPS; ++kk)
             ka[kk] = as_vec8<V8>(*reinterpret_cast<const uint4_t *>(stage + k_lane + 16 * kk));
     };
-    // S^T = K Q^T
+    // S^T = K Q^T.  Matrix instructions are issued at raised wave priority:
+    // the SIMD then starts a wave's next MFMA as soon as the matrix core is
+    // free and fills the gaps with the other waves' vector work.
     auto qk = [&](const V8 (&ka)[KSTEPS]) {
         float16_t s = float16_t{};
+        __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int kk = 0; kk < KSTEPS; ++kk) s = mfma32(ka[kk], qf[kk], s);
+        __builtin_amdgcn_s_setprio(0);
         return s;
     };
     auto scores = [&](const unsigned short *stage) {
@@ -259,11 +265,13 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
     // O^T += V^T P^T with the weights of one tile (k-step j = keys 16 j .. 16 j
     // + 15 of the wave's half)
     auto pv = [&](const half8_t &p0, const half8_t &p1, const half8_t (&va)[KSTEPS]) {
+        __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
             oacc[dt] = mfma32(va[2 * dt], p0, oacc[dt]);
             oacc[dt] = mfma32(va[2 * dt + 1], p1, oacc[dt]);
         }
+        __builtin_amdgcn_s_setprio(0);
     };
 
     // hide keys of tile t that some row of the wave must not see
