@@ -30,8 +30,10 @@
 // skipped on most tiles; sum and accumulator always share the base, so the
 // result is unchanged.
 // A wave's steps run in order; latency is hidden by running several
-// workgroups per CU (two: four waves per SIMD at D = 64 within 128 VGPRs; two
-// 4-wave workgroups at D = 128), whose barriers are independent.
+// workgroups per CU (two 8-wave ones at D = 64: four waves per SIMD within 128
+// VGPRs; three 4-wave ones at D = 128: three waves per SIMD within 168 VGPRs),
+// whose barriers are independent.  Matrix instructions are issued at raised
+// wave priority.
 // Masked scores are -inf and give exactly 0 (the exponent factor is kept
 // strictly positive, also for scale = 0).  Keys past the end read as zero
 // (buffer loads with the tensor's extent as the range) and are masked.
@@ -66,12 +68,13 @@ struct PrefillArgs {
 // a tile.  D = 64: two waves per slot (64-key tiles, key halves merged at the
 // end), 8-wave workgroups of at most 128 VGPRs, two per CU (four waves per
 // SIMD).  D = 128: the accumulator (64 VGPRs) and Q (32) leave no room for
-// that, so one wave per slot (32-key tiles) and 4-wave workgroups, two per CU
-// (two waves per SIMD, from independent workgroups).  Two LDS stages in both.
+// that, so one wave per slot (32-key tiles) and 4-wave workgroups, three per
+// CU (three waves per SIMD, from independent workgroups; operands are read
+// from LDS in small groups to fit 168 VGPRs).  Two LDS stages in both.
 template <int D> struct Cfg {
     static constexpr int NQ = D == 64 ? 2 : 1;       // waves per slot
-    static constexpr int WPE = D == 64 ? 4 : 2;      // waves per SIMD
-    static constexpr int WPC = D == 64 ? 2 : 2;      // workgroups per CU
+    static constexpr int WPE = D == 64 ? 4 : 3;      // waves per SIMD
+    static constexpr int WPC = D == 64 ? 2 : 3;      // workgroups per CU
     static constexpr int BC = 32 * NQ;               // keys per tile
     static constexpr int NT = 64 * NSLOT * NQ;       // threads per workgroup
     static constexpr int NSTAGE = 2;                 // LDS tile stages
@@ -274,6 +277,51 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
         __builtin_amdgcn_s_setprio(0);
     };
 
+    // Grouped operand reads for D = 128: two k-steps per group, the next
+    // group read from LDS while the current one multiplies, so that at most
+    // four operand words are live instead of one per k-step (this keeps the
+    // kernel within the 168 VGPRs of three waves per SIMD).
+    auto scores_jit = [&](const unsigned short *stage) {
+        float16_t s = float16_t{};
+        V8 cur0, cur1, nxt0, nxt1;
+        cur0 = as_vec8<V8>(*reinterpret_cast<const uint4_t *>(stage + k_lane));
+        cur1 = as_vec8<V8>(*reinterpret_cast<const uint4_t *>(stage + k_lane + 16));
+        __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+        for (int g = 0; g < KSTEPS / 2; ++g) {
+            if (g + 1 < KSTEPS / 2) {
+                nxt0 = as_vec8<V8>(*reinterpret_cast<const uint4_t *>(stage + k_lane + 32 * (g + 1)));
+                nxt1 = as_vec8<V8>(*reinterpret_cast<const uint4_t *>(stage + k_lane + 32 * (g + 1) + 16));
+            }
+            s = mfma32(cur0, qf[2 * g], s);
+            s = mfma32(cur1, qf[2 * g + 1], s);
+            __builtin_amdgcn_sched_barrier(0);
+            cur0 = nxt0;
+            cur1 = nxt1;
+        }
+        __builtin_amdgcn_s_setprio(0);
+        return s;
+    };
+    auto pv_jit = [&](const half8_t &p0, const half8_t &p1, const unsigned short *stage) {
+        half8_t cur0, cur1, nxt0, nxt1;
+        cur0 = as_vec8<half8_t>(*reinterpret_cast<const uint4_t *>(stage + v_lane));
+        cur1 = as_vec8<half8_t>(*reinterpret_cast<const uint4_t *>(stage + v_lane + 16));
+        __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+            if (dt + 1 < DT) {
+                nxt0 = as_vec8<half8_t>(*reinterpret_cast<const uint4_t *>(stage + v_lane + 32 * (dt + 1) * SM::VTS));
+                nxt1 = as_vec8<half8_t>(*reinterpret_cast<const uint4_t *>(stage + v_lane + 32 * (dt + 1) * SM::VTS + 16));
+            }
+            oacc[dt] = mfma32(cur0, p0, oacc[dt]);
+            oacc[dt] = mfma32(cur1, p1, oacc[dt]);
+            __builtin_amdgcn_sched_barrier(0);
+            cur0 = nxt0;
+            cur1 = nxt1;
+        }
+        __builtin_amdgcn_s_setprio(0);
+    };
+
     // hide keys of tile t that some row of the wave must not see
     auto mask = [&](float16_t &s, int t) {
         const int kw = t * BC + 32 * kh;        // first key of this wave's half
@@ -355,14 +403,26 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
     auto step = [&](int i, auto R) {   // R: stage of tile i (i % 2)
         constexpr int r = decltype(R)::value;
         const bool more = i + 1 < ntiles;
-        if (more) gload((i + 1) * BC);
-        float16_t s = scores(stage_at(r));
+        float16_t s;
+        if constexpr (D == 128) {
+            // next tile's loads after the K reads: their registers are then
+            // not live across the QK^T product
+            s = scores_jit(stage_at(r));
+            if (more) gload((i + 1) * BC);
+        } else {
+            if (more) gload((i + 1) * BC);
+            s = scores(stage_at(r));
+        }
         mask(s, i);
         half8_t p0, p1;
         softmax(s, p0, p1);
-        half8_t va[KSTEPS];
-        vread(stage_at(r), va);
-        pv(p0, p1, va);
+        if constexpr (D == 128) {
+            pv_jit(p0, p1, stage_at(r));
+        } else {
+            half8_t va[KSTEPS];
+            vread(stage_at(r), va);
+            pv(p0, p1, va);
+        }
         if (more) sstore(stage_at(r ^ 1));
         __syncthreads();
     };
