@@ -13,11 +13,13 @@
 //
 // Inside a workgroup each of the 4 waves streams its own 32-key chunks
 // (round robin over the split), carrying running max / sum / accumulator as
-// in Alg. 1 (tile-wise, with the lazy-rescale rule of the prefill kernel).
-// The waves' partial states are merged through LDS and the workgroup writes
-// one (unnormalised accumulator, max, sum) triple per query head and split.
-// A second kernel merges the splits of each (batch, query head) by their
-// log-sum-exp and applies the final 1/l normalisation.
+// in Alg. 1 (tile-wise; the running maximum only moves when a tile's maximum
+// exceeds it by more than 8 in the log2 domain).  A chunk's K and V rows are
+// loaded whole and staged in the wave's own LDS area, one chunk ahead of the
+// arithmetic.  The waves' partial states are merged through LDS and the
+// workgroup writes one (unnormalised accumulator, max, sum) triple per query
+// head and split.  A second kernel merges the splits of each (batch, query
+// head) by their log-sum-exp and applies the final 1/l normalisation.
 #include "fa_common.h"
 #include "fa_internal.h"
 
@@ -43,8 +45,9 @@ struct DecodeArgs {
 };
 
 template <int D> struct DSmem {
+    static constexpr int KS = D + 8;             // K row stride (16-bit elements)
     static constexpr int VS = D + 16;            // V row stride (16-bit elements)
-    static constexpr int WAVE = KPW * VS;        // per-wave V staging
+    static constexpr int WAVE = KPW * (KS + VS); // per-wave K and V staging
     static constexpr int MERGE_FLOATS = NW * QG * (D + 2);
     static constexpr int BYTES_STAGE = NW * WAVE * 2;
     static constexpr int BYTES = BYTES_STAGE > MERGE_FLOATS * 4 ? BYTES_STAGE : MERGE_FLOATS * 4;
@@ -64,7 +67,7 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
     constexpr int KST = D / 32;          // QK^T contraction steps (K = 32)
     constexpr int DT = D / 16;           // output row tiles of 16
     constexpr int CPR = D / 8;           // 16-byte chunks per key row
-    constexpr int VLOADS = KPW * CPR / 64;
+    constexpr int RLOADS = KPW * CPR / 64;   // 16-byte row loads per lane per chunk (K and V each)
     constexpr bool IN_BF16 = __is_same(TIN, bf16_t);
 
     __shared__ __attribute__((aligned(16))) unsigned char smem[SM::BYTES];
@@ -104,7 +107,8 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
     const size_t row_stride = (size_t)a.Hkv * D;                  // elements between keys
     const size_t head_off = ((size_t)b * Nk * a.Hkv + g) * D;     // key 0 of (b, g)
 
-    unsigned short *vst = reinterpret_cast<unsigned short *>(smem) + w * SM::WAVE;
+    unsigned short *kst = reinterpret_cast<unsigned short *>(smem) + w * SM::WAVE;
+    unsigned short *vst = kst + KPW * SM::KS;
     const _Float16 *vsth = reinterpret_cast<const _Float16 *>(vst);
     // transpose-read lane offset: rows 4*lg + (lc / 4), columns 4 * (lc % 4)
     const int v_lane = (4 * lg + (lc >> 2)) * SM::VS + 4 * (lc & 3);
@@ -114,32 +118,30 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
     for (int dt = 0; dt < DT; ++dt) oacc[dt] = float4_t{};
     float m_run = -INFINITY, l_run = 0.f;
 
-    uint4_t kr[2][KST], kn[2][KST];   // current / next chunk: [16-key half][k-step]
-    uint4_t vr[VLOADS];
+    // A chunk's K and V rows are loaded whole (64 lanes cover 64 / CPR
+    // complete rows per instruction, the access pattern that streams from HBM
+    // fastest) and staged in the wave's own LDS area: K as is (read back in
+    // the MFMA operand layout), V as fp16 (read back transposed).
+    uint4_t kr[RLOADS], vr[RLOADS];   // the next chunk's rows, in flight
     auto gload = [&](int kb) {
 #pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-            const int key = kb + 16 * hf + lc;
-#pragma unroll
-            for (int ks = 0; ks < KST; ++ks) {
-                kn[hf][ks] = uint4_t{0u, 0u, 0u, 0u};
-                if (key < k1)
-                    kn[hf][ks] = ld16_stream(kbase + head_off + key * row_stride + 32 * ks + 8 * lg);
-            }
-        }
-#pragma unroll
-        for (int i = 0; i < VLOADS; ++i) {
+        for (int i = 0; i < RLOADS; ++i) {
             const int c = l + 64 * i;
             const int key = kb + c / CPR, cc = c % CPR;
+            kr[i] = uint4_t{0u, 0u, 0u, 0u};
             vr[i] = uint4_t{0u, 0u, 0u, 0u};
-            if (key < k1) vr[i] = ld16_stream(vbase + head_off + key * row_stride + 8 * cc);
+            if (key < k1) {
+                kr[i] = ld16_stream(kbase + head_off + key * row_stride + 8 * cc);
+                vr[i] = ld16_stream(vbase + head_off + key * row_stride + 8 * cc);
+            }
         }
     };
-    auto vstore = [&]() {
+    auto kvstore = [&]() {
 #pragma unroll
-        for (int i = 0; i < VLOADS; ++i) {
+        for (int i = 0; i < RLOADS; ++i) {
             const int c = l + 64 * i;
             const int key = c / CPR, cc = c % CPR;
+            st16(kst + key * SM::KS + 8 * cc, kr[i]);
             st16(vst + key * SM::VS + 8 * cc, IN_BF16 ? bf16x8_to_f16x8(vr[i]) : vr[i]);
         }
     };
@@ -147,23 +149,21 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
     const int nchunks = (k1 > k0) ? (k1 - k0 + KPW - 1) / KPW : 0;
     if (w < nchunks) {
         gload(k0 + w * KPW);
-        vstore();
+        kvstore();
         wave_lds_fence();
     }
     for (int ch = w; ch < nchunks; ch += NW) {
         const int kb = k0 + ch * KPW;
         const bool more = ch + NW < nchunks;
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf)
-#pragma unroll
-            for (int ks = 0; ks < KST; ++ks) kr[hf][ks] = kn[hf][ks];
         if (more) gload(kb + NW * KPW);
         // ---- S^T = K Q^T: two 16-key halves, lane owns query lc, keys 4 lg + r
         float4_t s0 = float4_t{}, s1 = float4_t{};
+        const unsigned short *kl = kst + lc * SM::KS + 8 * lg;
 #pragma unroll
         for (int ks = 0; ks < KST; ++ks) {
-            s0 = mfma16(as_vec8<V8>(kr[0][ks]), qf[ks], s0);
-            s1 = mfma16(as_vec8<V8>(kr[1][ks]), qf[ks], s1);
+            s0 = mfma16(as_vec8<V8>(*reinterpret_cast<const uint4_t *>(kl + 32 * ks)), qf[ks], s0);
+            s1 = mfma16(as_vec8<V8>(*reinterpret_cast<const uint4_t *>(kl + 16 * SM::KS + 32 * ks)),
+                        qf[ks], s1);
         }
         const bool masked = kb + KPW > k1;
         if (masked) {
@@ -211,8 +211,8 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
             oacc[dt] = mfma16(va, pf, oacc[dt]);
         }
         if (more) {
-            wave_lds_fence();   // transpose reads of this chunk are done
-            vstore();
+            wave_lds_fence();   // operand reads of this chunk are done
+            kvstore();
             wave_lds_fence();
         }
     }
@@ -266,51 +266,48 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
 
 // Merge of the S partial results of one (batch, query head): lse-weighted sum
 // of the unnormalised accumulators, final normalisation, log-sum-exp output.
-// All loads of one phase are independent, so each phase costs one memory
-// round trip: (1) every split's max and sum, (2) the accumulator columns.
+// Splits are taken in groups of 16 whose loads are all issued together (one
+// memory round trip per group; the usual split counts fit in one group); the
+// running maximum moves once per group.  Every thread of the block handles
+// one output column and forms the same maximum and sum.
 template <typename TOUT, int D>
 __global__ __launch_bounds__(D) void decode_combine_kernel(const float *__restrict__ opart,
                                                           const float *__restrict__ mpart,
                                                           const float *__restrict__ lpart,
                                                           void *o, float *lse, int S) {
-    __shared__ float wgt[FA_MAX_SPLITS];
-    __shared__ float lsp[FA_MAX_SPLITS];
-    __shared__ float red[2 * (D / 64)];
-    const int bh = blockIdx.x, t = threadIdx.x, lane = t & 63, wv = t >> 6;
+    constexpr int CH = 16;
+    const int bh = blockIdx.x, t = threadIdx.x;
     const float *mp = mpart + (size_t)bh * S;
     const float *lp = lpart + (size_t)bh * S;
-    const float *op = opart + (size_t)bh * S * D;
-    float mloc = -INFINITY;
-    for (int s = t; s < S; s += D) {
-        const float m = mp[s];
-        wgt[s] = m;
-        lsp[s] = lp[s];
-        mloc = __builtin_fmaxf(mloc, m);
+    const float *op = opart + (size_t)bh * S * D + t;
+    float M = -INFINITY, L = 0.f, acc = 0.f;
+    for (int s0 = 0; s0 < S; s0 += CH) {
+        float mv[CH], lv[CH], ov[CH];
+#pragma unroll
+        for (int j = 0; j < CH; ++j) {
+            mv[j] = -INFINITY;
+            lv[j] = 0.f;
+            ov[j] = 0.f;
+            if (s0 + j < S) {
+                mv[j] = mp[s0 + j];
+                lv[j] = lp[s0 + j];
+                ov[j] = op[(size_t)(s0 + j) * D];
+            }
+        }
+        float Mc = M;
+#pragma unroll
+        for (int j = 0; j < CH; ++j) Mc = __builtin_fmaxf(Mc, mv[j]);
+        const float alpha = (M == -INFINITY) ? 0.f : exp2_fast(M - Mc);
+        L *= alpha;
+        acc *= alpha;
+#pragma unroll
+        for (int j = 0; j < CH; ++j) {
+            const float w = (mv[j] == -INFINITY) ? 0.f : exp2_fast(mv[j] - Mc);
+            L = __builtin_fmaf(w, lv[j], L);
+            acc = __builtin_fmaf(w, ov[j], acc);
+        }
+        M = Mc;
     }
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) mloc = __builtin_fmaxf(mloc, __shfl_xor(mloc, off));
-    if (lane == 0) red[wv] = mloc;
-    __syncthreads();
-    float M = red[0];
-#pragma unroll
-    for (int i = 1; i < D / 64; ++i) M = __builtin_fmaxf(M, red[i]);
-    float lsum = 0.f;
-    for (int s = t; s < S; s += D) {
-        const float m = wgt[s];
-        const float w = (m == -INFINITY) ? 0.f : exp2_fast(m - M);
-        wgt[s] = w;
-        lsum += w * lsp[s];
-    }
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) lsum += __shfl_xor(lsum, off);
-    if (lane == 0) red[D / 64 + wv] = lsum;
-    __syncthreads();
-    float L = 0.f;
-#pragma unroll
-    for (int i = 0; i < D / 64; ++i) L += red[D / 64 + i];
-    float acc = 0.f;
-#pragma unroll 8
-    for (int s = 0; s < S; ++s) acc += wgt[s] * op[(size_t)s * D + t];
     reinterpret_cast<TOUT *>(o)[(size_t)bh * D + t] = from_f32<TOUT>(acc / L);
     if (lse && t == 0) lse[bh] = (M + log2f(L)) * kLn2;
 }
