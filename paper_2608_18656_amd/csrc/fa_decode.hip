@@ -31,7 +31,7 @@ constexpr int NW = 4;          // waves per workgroup
 constexpr int QG = 16;         // query heads per MFMA column block
 constexpr float TAU = 8.0f;    // lazy-rescale threshold (log2 units)
 constexpr int MIN_KEYS_PER_SPLIT = 256;
-constexpr int TARGET_WORKGROUPS = 1024;
+constexpr int TARGET_WORKGROUPS = 256;   // about one workgroup per CU: long splits, few partials
 
 struct DecodeArgs {
     const void *q, *k, *v;
