@@ -415,12 +415,14 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
         }
         mask(s, i);
         half8_t p0, p1;
+        half8_t va[KSTEPS];
+        // D = 64: the V operands are read before the softmax, so that their
+        // LDS latency is not on the step's critical path
+        if constexpr (D == 64) vread(stage_at(r), va);
         softmax(s, p0, p1);
         if constexpr (D == 128) {
             pv_jit(p0, p1, stage_at(r));
         } else {
-            half8_t va[KSTEPS];
-            vread(stage_at(r), va);
             pv(p0, p1, va);
         }
         if (more) sstore(stage_at(r ^ 1));
