@@ -70,7 +70,7 @@ typedef enum {
     FA_ERR_ALIGN = 7,        /* a tensor pointer is not 16-byte aligned */
     FA_ERR_ALIAS = 8,        /* o or lse overlaps q, k, v, or each other */
     FA_ERR_DTYPE = 9,        /* unknown dtype, or out_dtype not in {in_dtype, FA_F32} */
-    FA_ERR_WORKSPACE = 10,   /* workspace allocation failed */
+    FA_ERR_WORKSPACE = 10,   /* workspace allocation failed, or the caller-set one is too small */
     FA_ERR_HIP = 11,         /* a HIP runtime call or kernel launch failed */
     FA_ERR_SPLITS = 12       /* num_splits outside [0, FA_MAX_SPLITS] */
 } fa_status_t;
@@ -124,6 +124,22 @@ size_t fa_workspace_bytes(int B, int Hq, int Hkv, int Nq, int Nk, int D, fa_dtyp
 /* Frees the library-owned workspace of the current device (synchronises the
  * device first).  Safe to call when none is held. */
 fa_status_t fa_release_workspace(void);
+
+/* Caller-owned decode workspace for the current device (the split-KV
+ * partial results of the decode path, which otherwise live in a
+ * library-owned, grow-only device buffer allocated on first use).
+ * dev_ptr: device memory on the current device, 16-byte aligned, at least
+ * `bytes` long, owned by the caller and left untouched by the library except
+ * as scratch during calls; it must stay allocated until it is replaced or
+ * cleared.  After a successful call every decode call on this device uses
+ * it and never allocates; a call that needs more than `bytes` (see
+ * fa_workspace_bytes) returns FA_ERR_WORKSPACE without launching anything.
+ * Calls sharing one workspace must be ordered (one stream, or synchronised
+ * streams).  fa_set_workspace(NULL, 0) returns the device to the
+ * library-owned workspace.  Errors: FA_ERR_NULL for a NULL pointer with
+ * bytes > 0 or a non-NULL pointer with bytes == 0, FA_ERR_ALIGN for a
+ * misaligned pointer, FA_ERR_HIP when the current device cannot be read. */
+fa_status_t fa_set_workspace(void *dev_ptr, size_t bytes);
 
 #ifdef __cplusplus
 }

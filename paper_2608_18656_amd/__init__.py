@@ -9,7 +9,7 @@ from __future__ import annotations
 import math
 
 __all__ = ["fwd", "fwd_splitkv", "FaError", "validate", "workspace_bytes", "release_workspace",
-           "version", "DTYPE_CODES"]
+           "set_workspace", "version", "DTYPE_CODES"]
 
 
 class FaError(RuntimeError):
@@ -134,6 +134,31 @@ def release_workspace():
 
     lib = _lib.load()
     _check(lib, lib.fa_release_workspace())
+
+
+_USER_WORKSPACE = {}   # device index -> caller tensor kept alive while set
+
+
+def set_workspace(buf=None):
+    """Use the device tensor ``buf`` (contiguous, on the current device) as
+    the decode workspace of its device, or return to the library-owned one
+    with ``None``; see fa_set_workspace in include/fa.h."""
+    from . import _lib
+
+    torch = _torch()
+    lib = _lib.load()
+    if buf is None:
+        dev = torch.cuda.current_device()
+        _check(lib, lib.fa_set_workspace(None, 0))
+        _USER_WORKSPACE.pop(dev, None)
+        return
+    if not buf.is_cuda or not buf.is_contiguous():
+        raise ValueError("workspace must be a contiguous device tensor")
+    if buf.device.index != torch.cuda.current_device():
+        raise ValueError("workspace must be on the current device")
+    nbytes = buf.numel() * buf.element_size()
+    _check(lib, lib.fa_set_workspace(buf.data_ptr() if nbytes else None, nbytes))
+    _USER_WORKSPACE[buf.device.index] = buf
 
 
 def version() -> tuple:

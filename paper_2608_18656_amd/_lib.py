@@ -24,7 +24,7 @@ STATUS_NAMES = {
 # Every symbol include/fa.h declares.
 EXPORTS = ("fa_status_string", "fa_version", "fa_validate", "fa_fwd_f16", "fa_fwd_bf16",
            "fa_fwd_f32", "fa_fwd", "fa_fwd_splitkv", "fa_workspace_bytes",
-           "fa_release_workspace")
+           "fa_release_workspace", "fa_set_workspace")
 
 _lib = None
 
@@ -62,5 +62,7 @@ def load():
     lib.fa_workspace_bytes.restype = ctypes.c_size_t
     lib.fa_release_workspace.argtypes = []
     lib.fa_release_workspace.restype = _I
+    lib.fa_set_workspace.argtypes = [_P, ctypes.c_size_t]
+    lib.fa_set_workspace.restype = _I
     _lib = lib
     return lib

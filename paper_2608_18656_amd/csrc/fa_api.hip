@@ -24,20 +24,29 @@ bool mul_ok(long long a, long long b, long long *r) {
     return true;
 }
 
-// Device workspace for the split-KV partial results (one per device).
+// Device workspace for the split-KV partial results (one per device):
+// library-owned and grow-only, unless the caller has set its own.
 struct Workspace {
     void *ptr = nullptr;
     size_t bytes = 0;
+    void *user = nullptr;       // caller-owned workspace (fa_set_workspace), or NULL
+    size_t user_bytes = 0;
 };
 constexpr int kMaxDevices = 64;
 Workspace g_ws[kMaxDevices];
 std::mutex g_ws_mu;
 
-fa_status_t get_workspace(size_t need, void **out) {
+fa_status_t get_workspace(size_t need, void **out, bool *user) {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return FA_ERR_HIP;
     std::lock_guard<std::mutex> lk(g_ws_mu);
     Workspace &w = g_ws[dev];
+    *user = w.user != nullptr;
+    if (w.user) {
+        if (w.user_bytes < need) return FA_ERR_WORKSPACE;
+        *out = w.user;
+        return FA_OK;
+    }
     if (w.bytes < need) {
         if (w.ptr) {
             // earlier calls may still be reading the old buffer
@@ -69,9 +78,18 @@ fa_status_t run(const void *q, const void *k, const void *v, void *o, float *lse
     hipError_t e;
     if (fa::decode_supported(Nq, D, in)) {
         const int S = splits_req > 0 ? splits_req : fa::decode_default_splits(B, Hq, Hkv, Nk, D);
+        const size_t need = fa::decode_workspace_bytes(B, Hq, D, S);
         void *ws = nullptr;
-        st = get_workspace(fa::decode_workspace_bytes(B, Hq, D, S), &ws);
+        bool user = false;
+        st = get_workspace(need, &ws, &user);
         if (st != FA_OK) return st;
+        if (user) {   // a caller-owned workspace must not overlap the call's tensors
+            const size_t qb = (size_t)B * Nq * Hq * D * esize(in), kb = (size_t)B * Nk * Hkv * D * esize(in);
+            const size_t ob = (size_t)B * Nq * Hq * D * esize(out), lb = (size_t)B * Hq * Nq * sizeof(float);
+            if (overlaps(ws, need, q, qb) || overlaps(ws, need, k, kb) || overlaps(ws, need, v, kb) ||
+                overlaps(ws, need, o, ob) || (lse && overlaps(ws, need, lse, lb)))
+                return FA_ERR_ALIAS;
+        }
         e = fa::launch_decode(p, S, ws, s);
     } else if (fa::prefill_supported(D, in)) {
         e = fa::launch_prefill(p, s);
@@ -97,7 +115,8 @@ const char *fa_status_string(fa_status_t s) {
     case FA_ERR_ALIGN: return "FA_ERR_ALIGN: a tensor pointer is misaligned";
     case FA_ERR_ALIAS: return "FA_ERR_ALIAS: o or lse overlaps another tensor";
     case FA_ERR_DTYPE: return "FA_ERR_DTYPE: unsupported dtype combination";
-    case FA_ERR_WORKSPACE: return "FA_ERR_WORKSPACE: workspace allocation failed";
+    case FA_ERR_WORKSPACE:
+        return "FA_ERR_WORKSPACE: workspace allocation failed, or the caller-set workspace is too small";
     case FA_ERR_HIP: return "FA_ERR_HIP: HIP runtime or launch error";
     case FA_ERR_SPLITS: return "FA_ERR_SPLITS: num_splits out of range";
     }
@@ -178,6 +197,17 @@ size_t fa_workspace_bytes(int B, int Hq, int Hkv, int Nq, int Nk, int D, fa_dtyp
     if (num_splits < 0 || num_splits > FA_MAX_SPLITS) return 0;
     const int S = num_splits > 0 ? num_splits : fa::decode_default_splits(B, Hq, Hkv, Nk, D);
     return fa::decode_workspace_bytes(B, Hq, D, S);
+}
+
+fa_status_t fa_set_workspace(void *dev_ptr, size_t bytes) {
+    if ((dev_ptr == nullptr) != (bytes == 0)) return FA_ERR_NULL;
+    if (reinterpret_cast<uintptr_t>(dev_ptr) & 15) return FA_ERR_ALIGN;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return FA_ERR_HIP;
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    g_ws[dev].user = dev_ptr;
+    g_ws[dev].user_bytes = bytes;
+    return FA_OK;
 }
 
 fa_status_t fa_release_workspace(void) {

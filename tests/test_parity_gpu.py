@@ -201,3 +201,38 @@ def test_decode_calls_with_changing_shapes():
         o, lse = gpu_attention(q, k, v, False, default_scale(D), out_dtype=torch.float32,
                                num_splits=S)
         check_against(o, lse, o_ref, l_ref, DTYPES[dt], True, f"call {i} {B}x{Hq}x{Hkv}")
+
+
+def test_caller_owned_workspace():
+    """fa_set_workspace: a caller buffer of exactly fa_workspace_bytes gives
+    bitwise the same result as the library-owned workspace; a smaller one is
+    refused with FA_ERR_WORKSPACE before any launch; one overlapping an
+    input is refused with FA_ERR_ALIAS; clearing returns to the library's."""
+    B, Hq, Hkv, Nk, D, S = 4, 32, 8, 1000, 128, 4
+    q, k, v = make_qkv(B, Hq, Hkv, 1, Nk, D, "bf16", seed=77)
+    qd, kd, vd = (t.cuda() for t in (q, k, v))
+    scale = default_scale(D)
+    o_lib, l_lib = fa.fwd(qd, kd, vd, scale=scale, num_splits=S, out_dtype=torch.float32)
+    need = fa.workspace_bytes(B, Hq, Hkv, 1, Nk, D, "bf16", S)
+    assert need > 0
+    buf = torch.empty(need, dtype=torch.uint8, device="cuda")
+    try:
+        fa.set_workspace(buf)
+        o_usr, l_usr = fa.fwd(qd, kd, vd, scale=scale, num_splits=S, out_dtype=torch.float32)
+        torch.cuda.synchronize()
+        assert torch.equal(o_usr, o_lib) and torch.equal(l_usr, l_lib)
+        fa.set_workspace(buf[: need - 16])
+        with pytest.raises(fa.FaError) as e:
+            fa.fwd(qd, kd, vd, scale=scale, num_splits=S)
+        assert e.value.status == 10
+        fa.set_workspace(kd.view(torch.uint8)[:need])
+        with pytest.raises(fa.FaError) as e:
+            fa.fwd(qd, kd, vd, scale=scale, num_splits=S)
+        assert e.value.status == 8
+    finally:
+        fa.set_workspace(None)
+    o_again, _ = fa.fwd(qd, kd, vd, scale=scale, num_splits=S, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert torch.equal(o_again, o_lib)
+    o_ref, l_ref = oracle.attention(q, k, v, False, scale)
+    check_against(o_usr, l_usr, o_ref, l_ref, DTYPES["bf16"], True, "caller workspace")
