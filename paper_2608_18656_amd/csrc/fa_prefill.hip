@@ -177,17 +177,26 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
 #pragma unroll
     for (int i = 0; i < SL; ++i) goff[i] = (int)((lkey(i) * row_elems + lcol(i)) * sizeof(S));
     uint4_t sr[SL];   // the next tile, in flight during a step
-    auto gload = [&](int kb) {   // tile starting at key kb (a multiple of BC)
-        // buffer view from the tile's first key to the end of the last key
-        // row: loads of keys past the end return zero (and are masked)
-        const S *tb = kvbase + (size_t)kb * row_elems;
-        const long long rem = ((long long)(Nk - 1 - kb) * (long long)row_elems + D) * (long long)sizeof(S);
-        const int nrec = (int)(rem < 0x7fffffffLL ? rem : 0x7fffffffLL);
+    // Scalar state of the next tile to load: its first key row, and the bytes
+    // from there to the end of the last key row (the buffer view, so that
+    // keys past the end read as zero); both advance by one tile per load.
+    const S *tnext = kvbase;
+    long long rem = (long long)(Nk - 1) * (long long)row_elems * (long long)sizeof(S) +
+                    (long long)D * (long long)sizeof(S);
+    auto gload = [&](int) {   // the next tile (tiles are loaded in order; the argument is its first key)
+        // view range, clamped to 31 bits (the tile's own extent always fits);
+        // the halves are opaque so that the test stays two 32-bit scalar
+        // compares instead of one 64-bit vector compare
+        unsigned rlo = (unsigned)rem, rhi = (unsigned)(rem >> 32);
+        asm volatile("" : "+s"(rlo), "+s"(rhi));
+        const int nrec = (int)(rhi != 0u ? 0x7fffffffu : __builtin_elementwise_min(rlo, 0x7fffffffu));
         const __amdgpu_buffer_rsrc_t rs =
-            __builtin_amdgcn_make_buffer_rsrc(const_cast<S *>(tb), (short)0, nrec, 0x00020000);
+            __builtin_amdgcn_make_buffer_rsrc(const_cast<S *>(tnext), (short)0, nrec, 0x00020000);
 #pragma unroll
         for (int i = 0; i < SL; ++i)
             sr[i] = __builtin_bit_cast(uint4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, goff[i], 0, 0));
+        tnext += (size_t)BC * row_elems;
+        rem -= (long long)BC * (long long)row_elems * (long long)sizeof(S);
     };
     // LDS destination (element offset inside a stage) of load i
     auto sdst = [&](int i) {
@@ -403,16 +412,11 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
     auto step = [&](int i, auto R) {   // R: stage of tile i (i % 2)
         constexpr int r = decltype(R)::value;
         const bool more = i + 1 < ntiles;
-        float16_t s;
-        if constexpr (D == 128) {
-            // next tile's loads after the K reads: their registers are then
-            // not live across the QK^T product
-            s = scores_jit(stage_at(r));
-            if (more) gload((i + 1) * BC);
-        } else {
-            if (more) gload((i + 1) * BC);
-            s = scores(stage_at(r));
-        }
+        // the next tile's loads are issued after the K operand reads (their
+        // scalar set-up then overlaps the LDS latency, and at D = 128 their
+        // registers are not live across the QK^T product)
+        float16_t s = D == 128 ? scores_jit(stage_at(r)) : scores(stage_at(r));
+        if (more) gload((i + 1) * BC);
         mask(s, i);
         half8_t p0, p1;
         half8_t va[KSTEPS];
