@@ -5,7 +5,8 @@
 // All arithmetic is fp32.  A workgroup of 256 threads owns 64 query rows of
 // one query head; four consecutive threads share a row and each holds an
 // interleaved quarter of its D columns (pairs d = 8 i + 2 t + {0, 1}).  Keys
-// are streamed in LDS tiles; per tile the scores of all tile keys are formed
+// are streamed in LDS tiles (the next tile's loads in flight during the
+// current one); per tile the scores of all tile keys are formed
 // (partial dot products reduced over the four threads of the row), then the
 // running maximum / sum / accumulator are updated once for the tile -- the
 // blocked form (Alg. 2) of the streaming recurrence of Alg. 1 -- and the
@@ -34,8 +35,8 @@ __global__ __launch_bounds__(256) void generic_kernel(GenericArgs a) {
     typedef typename Scalar<TIN>::type S;
     constexpr int KT = 16;                       // keys per LDS tile
     constexpr int NP = DMAX / 8;                 // column pairs per thread
-    __shared__ float ks[KT * DMAX];
-    __shared__ float vs[KT * DMAX];
+    __shared__ __attribute__((aligned(16))) float ks[KT * DMAX];
+    __shared__ __attribute__((aligned(16))) float vs[KT * DMAX];
 
     const int tid = threadIdx.x, row = tid >> 2, part = tid & 3;
     int bid = blockIdx.x;
@@ -65,21 +66,50 @@ __global__ __launch_bounds__(256) void generic_kernel(GenericArgs a) {
     const S *kb_ = reinterpret_cast<const S *>(a.k);
     const S *vb_ = reinterpret_cast<const S *>(a.v);
 
+    // Tile staging: each thread moves CH chunks of 4 consecutive columns of
+    // K and of V (chunk e = tid + 256 c: key e / (DMAX / 4), columns
+    // 4 (e % (DMAX / 4)) ..), converted to fp32; columns d >= D and keys past
+    // the end are zero-filled so the inner loops need no guard.  The next
+    // tile's loads are in flight while the current one is used.
+    constexpr int CPR4 = DMAX / 4;
+    constexpr int CH = (KT * CPR4 + 255) / 256;
+    float4_t kr[CH], vr[CH];
+    auto load4 = [&](const S *p) {
+        if constexpr (sizeof(S) == 4) {
+            return *reinterpret_cast<const float4_t *>(p);
+        } else {
+            typedef S s4 __attribute__((ext_vector_type(4)));
+            const s4 u = *reinterpret_cast<const s4 *>(p);
+            return float4_t{to_f32(u[0]), to_f32(u[1]), to_f32(u[2]), to_f32(u[3])};
+        }
+    };
+    auto load_tile = [&](int kb) {
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            const int e = tid + 256 * c, kk = e / CPR4, d = 4 * (e % CPR4), key = kb + kk;
+            kr[c] = float4_t{};
+            vr[c] = float4_t{};
+            if (kk < KT && key < Nk && d < D) {
+                const size_t o = ((size_t)((size_t)b * Nk + key) * a.Hkv + g) * D + d;
+                kr[c] = load4(kb_ + o);
+                vr[c] = load4(vb_ + o);
+            }
+        }
+    };
+    if (kend > 0) load_tile(0);
+
     for (int kb = 0; kb < kend; kb += KT) {
         __syncthreads();
-        // columns d >= D are zero-filled so the inner loops need no guard
-        for (int e = tid; e < KT * DMAX; e += 256) {
-            const int kk = e / DMAX, d = e % DMAX, key = kb + kk;
-            float kv = 0.f, vv = 0.f;
-            if (key < Nk && d < D) {
-                const size_t o = ((size_t)((size_t)b * Nk + key) * a.Hkv + g) * D + d;
-                kv = to_f32(kb_[o]);
-                vv = to_f32(vb_[o]);
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            const int e = tid + 256 * c, kk = e / CPR4, d = 4 * (e % CPR4);
+            if (kk < KT) {
+                *reinterpret_cast<float4_t *>(&ks[kk * DMAX + d]) = kr[c];
+                *reinterpret_cast<float4_t *>(&vs[kk * DMAX + d]) = vr[c];
             }
-            ks[kk * DMAX + d] = kv;
-            vs[kk * DMAX + d] = vv;
         }
         __syncthreads();
+        if (kb + KT < kend) load_tile(kb + KT);
         float x[KT];
         float tmax = -INFINITY;
 #pragma unroll
