@@ -11,7 +11,7 @@
 // (batch, key/value head, 16-head query group, split), so that enough
 // workgroups stream K/V from HBM to keep every CU busy.
 //
-// Inside a workgroup each of the 4 waves streams its own 32-key chunks
+// Inside a workgroup each of the 8 waves streams its own 32-key chunks
 // (round robin over the split), carrying running max / sum / accumulator as
 // in Alg. 1 (tile-wise; the running maximum only moves when a tile's maximum
 // exceeds it by more than 8 in the log2 domain).  A chunk's K and V rows are
@@ -27,7 +27,7 @@ namespace fa {
 namespace {
 
 constexpr int KPW = 32;        // keys per wave iteration
-constexpr int NW = 4;          // waves per workgroup
+constexpr int NW = 8;          // waves per workgroup
 constexpr int QG = 16;         // query heads per MFMA column block
 constexpr float TAU = 8.0f;    // lazy-rescale threshold (log2 units)
 constexpr int MIN_KEYS_PER_SPLIT = 256;
@@ -60,7 +60,7 @@ __device__ __forceinline__ void wave_lds_fence() {
 }
 
 template <typename TIN, int D>
-__global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(64 * NW, 1) void decode_split_kernel(DecodeArgs a) {
     using S = typename TIN::scalar;
     using V8 = typename TIN::vec8;
     using SM = DSmem<D>;
@@ -217,7 +217,7 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
         }
     }
 
-    // ---- merge the four waves' partial states through LDS
+    // ---- merge the waves' partial states through LDS
     l_run += __shfl_xor(l_run, 16);
     l_run += __shfl_xor(l_run, 32);
     __syncthreads();
@@ -232,10 +232,10 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
         mine[D + 1] = l_run;
     }
     __syncthreads();
-    // 256 threads: query column tid / 16, 16 threads per query, D / 16 columns each
+    // the first 256 threads: query column tid / 16, 16 threads per query, D / 16 columns each
     const int mq = tid >> 4, part = tid & 15;
     const int mh = qg * QG + mq;
-    if (mh < G) {
+    if (mq < QG && mh < G) {
         float M = -INFINITY;
 #pragma unroll
         for (int ww = 0; ww < NW; ++ww) M = __builtin_fmaxf(M, mf[(ww * QG + mq) * (D + 2) + D]);
@@ -330,7 +330,7 @@ hipError_t launch_t(const Problem &p, int S, void *ws, hipStream_t stream) {
     a.qsign = p.scale < 0.f ? 0x80008000u : 0u;
     const long long nblocks = (long long)p.B * p.Hkv * a.nqg * S;
     if (nblocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL((decode_split_kernel<TIN, D>), dim3((unsigned)nblocks), dim3(256), 0,
+    hipLaunchKernelGGL((decode_split_kernel<TIN, D>), dim3((unsigned)nblocks), dim3(64 * NW), 0,
                        stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
