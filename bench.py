@@ -84,7 +84,7 @@ def time_calls(torch, fns, steps, warmup):
     return t0.elapsed_time(t1) / steps
 
 
-def run_workload(torch, fa, w, steps, warmup, kv_sets=1, num_splits=None):
+def run_workload(torch, fa, w, steps, warmup, kv_sets=1, num_splits=None, packing=None):
     from paper_2608_18656_amd.inputs import make_workload
 
     q, k, v = make_workload(w)
@@ -99,7 +99,7 @@ def run_workload(torch, fa, w, steps, warmup, kv_sets=1, num_splits=None):
     def make(i):
         qd, kd, vd = sets[i]
         return lambda: fa.fwd(qd, kd, vd, causal=w.causal, scale=w.softmax_scale, out=outs[i],
-                              lse=lses[i], num_splits=num_splits)
+                              lse=lses[i], num_splits=num_splits, heads_per_workgroup=packing)
 
     ms = time_calls(torch, [make(i) for i in range(len(sets))], steps, warmup)
     return ms, sets[0], outs[0], lses[0]
@@ -223,6 +223,23 @@ def main():
                                  "algorithmic_per_launch": x.kv_bytes()}}
             log(f"[bench] {name}: {xms * 1e3:.1f} us/call, {val:.1f} {u} ({100 * val / pk:.1f}%)")
             torch.cuda.empty_cache()
+        # inter-head packing ablation: the default schedule (the G query heads
+        # of a K/V group share each staged K/V tile) against the per-head one
+        ablation = []
+        for name in ("gqa_prefill_bf16", "gqa_prefill_d128_f16", "mqa_prefill_f16"):
+            x = WORKLOADS[name]
+            steps = max(5, min(args.steps, 20))
+            row = {"workload": name}
+            for label, hw in (("packed", None), ("per_head", 1)):
+                xms, *_ = run_workload(torch, fa, x, steps, 3, packing=hw)
+                row[label + "_us"] = round(xms * 1e3, 2)
+                row[label + "_tflops"] = round(x.flops() / (xms * 1e-3) / 1e12, 1)
+                torch.cuda.empty_cache()
+            row["speedup"] = round(row["per_head_us"] / row["packed_us"], 3)
+            ablation.append(row)
+            log(f"[bench] packing {name}: packed {row['packed_us']} us, per-head "
+                f"{row['per_head_us']} us ({row['speedup']}x)")
+        result["packing_ablation"] = ablation
         # achievable HBM bandwidth for context: a plain 1 GiB device copy
         src = torch.empty(1 << 29, dtype=torch.float16, device="cuda").fill_(1.0)
         dst = torch.empty_like(src)

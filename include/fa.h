@@ -72,7 +72,8 @@ typedef enum {
     FA_ERR_DTYPE = 9,        /* unknown dtype, or out_dtype not in {in_dtype, FA_F32} */
     FA_ERR_WORKSPACE = 10,   /* workspace allocation failed, or the caller-set one is too small */
     FA_ERR_HIP = 11,         /* a HIP runtime call or kernel launch failed */
-    FA_ERR_SPLITS = 12       /* num_splits outside [0, FA_MAX_SPLITS] */
+    FA_ERR_SPLITS = 12,      /* num_splits outside [0, FA_MAX_SPLITS] */
+    FA_ERR_PACKING = 13      /* heads_per_workgroup not 0, 1, 2 or 4, or not a divisor of Hq / Hkv */
 } fa_status_t;
 
 #define FA_MAX_SPLITS 256
@@ -115,6 +116,23 @@ fa_status_t fa_fwd_splitkv(const void *q, const void *k, const void *v, void *o,
                            int B, int Hq, int Hkv, int Nq, int Nk, int D, int causal,
                            float scale, void *stream, fa_dtype_t in_dtype,
                            fa_dtype_t out_dtype, int num_splits);
+
+/* Prefill with an explicit query-head packing (the inter-head packing of
+ * Sec. 4.1.1 and the GQA K/V reuse of Sec. 4.1.2 (iv)).  A prefill workgroup
+ * owns four 32-row query slots that read one key/value head;
+ * heads_per_workgroup of them are different query heads of that key/value
+ * group (at the same rows), so each K/V tile staged in LDS serves that many
+ * heads, and the rest are consecutive row blocks.  1 is the per-head
+ * schedule (four consecutive row blocks of one head); 0 picks what fa_fwd
+ * uses (4 when 4 divides Hq / Hkv, else 2 when 2 does, else 1).  The result
+ * is the same, bit for bit, for every packing.  Only the fp16 / bf16 prefill
+ * kernels (Nq > 1, D in {64, 128}) take the packing; other calls ignore it.
+ * Errors: FA_ERR_PACKING for a value other than 0, 1, 2, 4 or one that does
+ * not divide Hq / Hkv; otherwise as fa_fwd. */
+fa_status_t fa_fwd_packed(const void *q, const void *k, const void *v, void *o, float *lse,
+                          int B, int Hq, int Hkv, int Nq, int Nk, int D, int causal,
+                          float scale, void *stream, fa_dtype_t in_dtype,
+                          fa_dtype_t out_dtype, int heads_per_workgroup);
 
 /* Bytes of decode workspace a call with these sizes needs (0 when the call
  * takes no split-KV path).  num_splits as in fa_fwd_splitkv. */

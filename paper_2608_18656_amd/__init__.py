@@ -69,7 +69,8 @@ def _prepare(q, k, v, out, lse, out_dtype, return_lse):
 
 
 def fwd(q, k, v, causal: bool = False, scale: float | None = None, out=None, lse=None,
-        out_dtype=None, return_lse: bool = True, num_splits: int | None = None):
+        out_dtype=None, return_lse: bool = True, num_splits: int | None = None,
+        heads_per_workgroup: int | None = None):
     """Attention forward o = softmax(scale * q k^T) v on the GPU.
 
     q [B, Nq, Hq, D], k and v [B, Nk, Hkv, D] (contiguous, same dtype and
@@ -78,7 +79,9 @@ def fwd(q, k, v, causal: bool = False, scale: float | None = None, out=None, lse
     query i iff j <= i + Nk - Nq).  ``scale`` defaults to 1/sqrt(D).
     ``out_dtype=torch.float32`` returns the kernel's fp32 result before the
     final rounding.  ``num_splits`` forces the decode split count (decode
-    shapes only).  Returns (out, lse) with lse [B, Hq, Nq] float32 natural-log
+    shapes only); ``heads_per_workgroup`` (1, 2 or 4) forces the prefill
+    query-head packing (see fa_fwd_packed).  Returns (out, lse) with lse
+    [B, Hq, Nq] float32 natural-log
     log-sum-exp (None if return_lse is False and no lse tensor was given).
     """
     from . import _lib
@@ -94,10 +97,14 @@ def fwd(q, k, v, causal: bool = False, scale: float | None = None, out=None, lse
             lse.data_ptr() if lse is not None else None, B, Hq, Hkv, Nq, Nk, D,
             int(bool(causal)), float(scale), stream, codes[q.dtype], codes.get(odt, -1))
     with torch.cuda.device(q.device):
-        if num_splits is None:
-            st = lib.fa_fwd(*args)
-        else:
+        if num_splits is not None and heads_per_workgroup is not None:
+            raise ValueError("num_splits and heads_per_workgroup are exclusive")
+        if num_splits is not None:
             st = lib.fa_fwd_splitkv(*args, int(num_splits))
+        elif heads_per_workgroup is not None:
+            st = lib.fa_fwd_packed(*args, int(heads_per_workgroup))
+        else:
+            st = lib.fa_fwd(*args)
     _check(lib, st)
     return out, lse
 

@@ -19,12 +19,13 @@ STATUS_NAMES = {
     0: "FA_OK", 1: "FA_ERR_NULL", 2: "FA_ERR_DIM", 3: "FA_ERR_GQA_RATIO", 4: "FA_ERR_HEAD_DIM",
     5: "FA_ERR_CAUSAL_SHAPE", 6: "FA_ERR_SCALE", 7: "FA_ERR_ALIGN", 8: "FA_ERR_ALIAS",
     9: "FA_ERR_DTYPE", 10: "FA_ERR_WORKSPACE", 11: "FA_ERR_HIP", 12: "FA_ERR_SPLITS",
+    13: "FA_ERR_PACKING",
 }
 
 # Every symbol include/fa.h declares.
 EXPORTS = ("fa_status_string", "fa_version", "fa_validate", "fa_fwd_f16", "fa_fwd_bf16",
            "fa_fwd_f32", "fa_fwd", "fa_fwd_splitkv", "fa_workspace_bytes",
-           "fa_release_workspace", "fa_set_workspace")
+           "fa_release_workspace", "fa_set_workspace", "fa_fwd_packed")
 
 _lib = None
 
@@ -58,6 +59,8 @@ def load():
     lib.fa_fwd.restype = _I
     lib.fa_fwd_splitkv.argtypes = [_P, _P, _P, _P, _P] + _DIMS + [_P, _I, _I, _I]
     lib.fa_fwd_splitkv.restype = _I
+    lib.fa_fwd_packed.argtypes = [_P, _P, _P, _P, _P] + _DIMS + [_P, _I, _I, _I]
+    lib.fa_fwd_packed.restype = _I
     lib.fa_workspace_bytes.argtypes = [_I] * 6 + [_I, _I]
     lib.fa_workspace_bytes.restype = ctypes.c_size_t
     lib.fa_release_workspace.argtypes = []

@@ -69,11 +69,14 @@ fa_status_t get_workspace(size_t need, void **out, bool *user) {
 
 fa_status_t run(const void *q, const void *k, const void *v, void *o, float *lse, int B, int Hq,
                 int Hkv, int Nq, int Nk, int D, int causal, float scale, void *stream,
-                fa_dtype_t in, fa_dtype_t out, int splits_req) {
+                fa_dtype_t in, fa_dtype_t out, int splits_req, int hw_req = 0) {
     fa_status_t st = fa_validate(q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, in, out);
     if (st != FA_OK) return st;
     if (splits_req < 0 || splits_req > FA_MAX_SPLITS) return FA_ERR_SPLITS;
-    fa::Problem p{q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, in, out};
+    if (!(hw_req == 0 || hw_req == 1 || hw_req == 2 || hw_req == 4) ||
+        (hw_req > 0 && (Hq / Hkv) % hw_req != 0))
+        return FA_ERR_PACKING;
+    fa::Problem p{q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, in, out, hw_req};
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     hipError_t e;
     if (fa::decode_supported(Nq, D, in)) {
@@ -119,6 +122,8 @@ const char *fa_status_string(fa_status_t s) {
         return "FA_ERR_WORKSPACE: workspace allocation failed, or the caller-set workspace is too small";
     case FA_ERR_HIP: return "FA_ERR_HIP: HIP runtime or launch error";
     case FA_ERR_SPLITS: return "FA_ERR_SPLITS: num_splits out of range";
+    case FA_ERR_PACKING:
+        return "FA_ERR_PACKING: heads_per_workgroup must be 0, 1, 2 or 4 and divide Hq / Hkv";
     }
     return "unknown fa_status_t";
 }
@@ -188,6 +193,14 @@ fa_status_t fa_fwd_splitkv(const void *q, const void *k, const void *v, void *o,
                            int num_splits) {
     return run(q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, stream, in_dtype, out_dtype,
                num_splits);
+}
+
+fa_status_t fa_fwd_packed(const void *q, const void *k, const void *v, void *o, float *lse,
+                          int B, int Hq, int Hkv, int Nq, int Nk, int D, int causal, float scale,
+                          void *stream, fa_dtype_t in_dtype, fa_dtype_t out_dtype,
+                          int heads_per_workgroup) {
+    return run(q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, stream, in_dtype, out_dtype,
+               0, heads_per_workgroup);
 }
 
 size_t fa_workspace_bytes(int B, int Hq, int Hkv, int Nq, int Nk, int D, fa_dtype_t in_dtype,

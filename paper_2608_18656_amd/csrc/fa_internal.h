@@ -17,6 +17,7 @@ struct Problem {
     int causal;
     float scale;
     fa_dtype_t in, out;
+    int hw;   // prefill query heads per workgroup (0: the default choice)
 };
 
 // Each launcher enqueues its kernels on `stream` and returns the first HIP

@@ -516,7 +516,7 @@ hipError_t launch_t(const Problem &p, hipStream_t stream) {
     a.c = __builtin_fmaxf(__builtin_fabsf(p.scale), 1e-30f) * kLog2e;
     a.qsign = p.scale < 0.f ? 0x80008000u : 0u;
     const int G = p.Hq / p.Hkv;
-    a.HW = (NSLOT % 4 == 0 && G % 4 == 0) ? 4 : (G % 2 == 0 ? 2 : 1);
+    a.HW = p.hw > 0 ? p.hw : ((NSLOT % 4 == 0 && G % 4 == 0) ? 4 : (G % 2 == 0 ? 2 : 1));
     const int RB = NSLOT / a.HW;
     a.nmb = (p.Nq + WR * RB - 1) / (WR * RB);
     a.nhg = G / a.HW;

@@ -96,3 +96,13 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(_lib, "_lib", None)
     with pytest.raises(FileNotFoundError):
         _lib.load()
+
+
+@pytest.mark.parametrize("packing,Hq,Hkv", [(3, 4, 2), (-1, 4, 2), (8, 8, 1), (4, 4, 2), (2, 6, 2)])
+def test_packing_rejected_before_any_launch(packing, Hq, Hkv):
+    """fa_fwd_packed checks heads_per_workgroup on the host (no HIP call):
+    it must be 0, 1, 2 or 4 and divide Hq / Hkv."""
+    lib = _lib.load()
+    st = lib.fa_fwd_packed(GOOD["q"], GOOD["k"], GOOD["v"], GOOD["o"], GOOD["lse"], 1, Hq, Hkv,
+                           8, 8, 64, 1, 0.125, None, 0, 0, packing)
+    assert st == 13
