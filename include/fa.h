@@ -134,6 +134,25 @@ fa_status_t fa_fwd_packed(const void *q, const void *k, const void *v, void *o, 
                           float scale, void *stream, fa_dtype_t in_dtype,
                           fa_dtype_t out_dtype, int heads_per_workgroup);
 
+/* Attention against a key/value cache with per-sequence lengths (decode,
+ * and chunked prefill of Nq new tokens).  k and v are [B][Nk][Hkv][D]
+ * caches of which the first seqlens_k[b] rows of batch element b are valid;
+ * seqlens_k is a device array of B int32 values (read by the kernels; values
+ * are clamped to [0, Nk]).  The Nq queries of batch element b are the last
+ * Nq positions of its sequence: with causal = 1, query i sees keys
+ * j <= i + seqlens_k[b] - Nq (the bottom-right alignment of fa_fwd applied to
+ * each sequence).  A query row that sees no key (causal with
+ * seqlens_k[b] < Nq, or seqlens_k[b] = 0) gets 0 and a log-sum-exp of -inf.
+ * With seqlens_k[b] = Nk for every b the result equals fa_fwd's bit for bit.
+ * Decode calls (Nq = 1) take the split-KV path with the workspace of
+ * fa_workspace_bytes(…, Nk, …).  Errors: FA_ERR_NULL for a NULL seqlens_k,
+ * FA_ERR_ALIGN if it is not 4-byte aligned, FA_ERR_ALIAS if o or lse overlaps
+ * it; otherwise as fa_fwd (with Nk the cache length). */
+fa_status_t fa_fwd_kvcache(const void *q, const void *k, const void *v, void *o, float *lse,
+                           const int *seqlens_k, int B, int Hq, int Hkv, int Nq, int Nk, int D,
+                           int causal, float scale, void *stream, fa_dtype_t in_dtype,
+                           fa_dtype_t out_dtype);
+
 /* Bytes of decode workspace a call with these sizes needs (0 when the call
  * takes no split-KV path).  num_splits as in fa_fwd_splitkv. */
 size_t fa_workspace_bytes(int B, int Hq, int Hkv, int Nq, int Nk, int D, fa_dtype_t in_dtype,

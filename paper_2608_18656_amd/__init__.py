@@ -8,7 +8,7 @@ from __future__ import annotations
 
 import math
 
-__all__ = ["fwd", "fwd_splitkv", "FaError", "validate", "workspace_bytes", "release_workspace",
+__all__ = ["fwd", "fwd_splitkv", "fwd_kvcache", "FaError", "validate", "workspace_bytes", "release_workspace",
            "set_workspace", "version", "DTYPE_CODES"]
 
 
@@ -105,6 +105,35 @@ def fwd(q, k, v, causal: bool = False, scale: float | None = None, out=None, lse
             st = lib.fa_fwd_packed(*args, int(heads_per_workgroup))
         else:
             st = lib.fa_fwd(*args)
+    _check(lib, st)
+    return out, lse
+
+
+def fwd_kvcache(q, k_cache, v_cache, seqlens_k, causal: bool = False, scale: float | None = None,
+                out=None, lse=None, out_dtype=None, return_lse: bool = True):
+    """Attention against K/V caches [B, Nk, Hkv, D] of which the first
+    ``seqlens_k[b]`` rows are valid (``seqlens_k``: int32 [B] on the same
+    device); q [B, Nq, Hq, D] holds each sequence's last Nq positions (decode
+    for Nq = 1, chunked prefill otherwise).  Rows that see no key give 0 and
+    lse -inf.  See fa_fwd_kvcache in include/fa.h."""
+    from . import _lib
+
+    lib = _lib.load()
+    torch = _torch()
+    (B, Hq, Hkv, Nq, Nk, D), out, lse, odt = _prepare(q, k_cache, v_cache, out, lse, out_dtype,
+                                                      return_lse)
+    if (not seqlens_k.is_cuda or seqlens_k.dtype != torch.int32 or tuple(seqlens_k.shape) != (B,)
+            or not seqlens_k.is_contiguous() or seqlens_k.device != q.device):
+        raise ValueError("seqlens_k must be a contiguous int32 [B] tensor on q's device")
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    codes = _codes()
+    stream = torch.cuda.current_stream(q.device).cuda_stream
+    with torch.cuda.device(q.device):
+        st = lib.fa_fwd_kvcache(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), out.data_ptr(),
+                                lse.data_ptr() if lse is not None else None, seqlens_k.data_ptr(),
+                                B, Hq, Hkv, Nq, Nk, D, int(bool(causal)), float(scale), stream,
+                                codes[q.dtype], codes.get(odt, -1))
     _check(lib, st)
     return out, lse
 

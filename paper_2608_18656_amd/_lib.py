@@ -25,7 +25,7 @@ STATUS_NAMES = {
 # Every symbol include/fa.h declares.
 EXPORTS = ("fa_status_string", "fa_version", "fa_validate", "fa_fwd_f16", "fa_fwd_bf16",
            "fa_fwd_f32", "fa_fwd", "fa_fwd_splitkv", "fa_workspace_bytes",
-           "fa_release_workspace", "fa_set_workspace", "fa_fwd_packed")
+           "fa_release_workspace", "fa_set_workspace", "fa_fwd_packed", "fa_fwd_kvcache")
 
 _lib = None
 
@@ -61,6 +61,8 @@ def load():
     lib.fa_fwd_splitkv.restype = _I
     lib.fa_fwd_packed.argtypes = [_P, _P, _P, _P, _P] + _DIMS + [_P, _I, _I, _I]
     lib.fa_fwd_packed.restype = _I
+    lib.fa_fwd_kvcache.argtypes = [_P, _P, _P, _P, _P, _P] + _DIMS + [_P, _I, _I]
+    lib.fa_fwd_kvcache.restype = _I
     lib.fa_workspace_bytes.argtypes = [_I] * 6 + [_I, _I]
     lib.fa_workspace_bytes.restype = ctypes.c_size_t
     lib.fa_release_workspace.argtypes = []

@@ -69,14 +69,15 @@ fa_status_t get_workspace(size_t need, void **out, bool *user) {
 
 fa_status_t run(const void *q, const void *k, const void *v, void *o, float *lse, int B, int Hq,
                 int Hkv, int Nq, int Nk, int D, int causal, float scale, void *stream,
-                fa_dtype_t in, fa_dtype_t out, int splits_req, int hw_req = 0) {
+                fa_dtype_t in, fa_dtype_t out, int splits_req, int hw_req = 0,
+                const int *seqlens = nullptr) {
     fa_status_t st = fa_validate(q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, in, out);
     if (st != FA_OK) return st;
     if (splits_req < 0 || splits_req > FA_MAX_SPLITS) return FA_ERR_SPLITS;
     if (!(hw_req == 0 || hw_req == 1 || hw_req == 2 || hw_req == 4) ||
         (hw_req > 0 && (Hq / Hkv) % hw_req != 0))
         return FA_ERR_PACKING;
-    fa::Problem p{q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, in, out, hw_req};
+    fa::Problem p{q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, in, out, hw_req, seqlens};
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     hipError_t e;
     if (fa::decode_supported(Nq, D, in)) {
@@ -201,6 +202,22 @@ fa_status_t fa_fwd_packed(const void *q, const void *k, const void *v, void *o, 
                           int heads_per_workgroup) {
     return run(q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, stream, in_dtype, out_dtype,
                0, heads_per_workgroup);
+}
+
+fa_status_t fa_fwd_kvcache(const void *q, const void *k, const void *v, void *o, float *lse,
+                           const int *seqlens_k, int B, int Hq, int Hkv, int Nq, int Nk, int D,
+                           int causal, float scale, void *stream, fa_dtype_t in_dtype,
+                           fa_dtype_t out_dtype) {
+    if (!seqlens_k) return FA_ERR_NULL;
+    if (reinterpret_cast<uintptr_t>(seqlens_k) & 3) return FA_ERR_ALIGN;
+    if (B >= 1 && o && Hq >= 1 && Nq >= 1 && D >= 1) {
+        const size_t ob = (size_t)B * Nq * Hq * D * esize(out_dtype);
+        if (overlaps(o, ob, seqlens_k, (size_t)B * sizeof(int)) ||
+            (lse && overlaps(lse, (size_t)B * Hq * Nq * sizeof(float), seqlens_k, (size_t)B * sizeof(int))))
+            return FA_ERR_ALIAS;
+    }
+    return run(q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, stream, in_dtype, out_dtype, 0,
+               0, seqlens_k);
 }
 
 size_t fa_workspace_bytes(int B, int Hq, int Hkv, int Nq, int Nk, int D, fa_dtype_t in_dtype,

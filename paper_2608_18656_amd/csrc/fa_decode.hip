@@ -42,6 +42,7 @@ struct DecodeArgs {
     int nqg;        // 16-head query groups per key/value head
     float c;        // |scale| * log2(e)
     unsigned qsign; // sign flip of q for negative scale
+    const int *seqlens;   // valid keys per batch element (NULL: Nk for all)
 };
 
 template <int D> struct DSmem {
@@ -82,7 +83,8 @@ __global__ __launch_bounds__(64 * NW, 1) void decode_split_kernel(DecodeArgs a) 
     const int g = bid % a.Hkv;
     const int b = bid / a.Hkv;
     const int G = a.Hq / a.Hkv;
-    const int Nk = a.Nk;
+    // valid keys of this batch element (a cache of a.Nk rows per element)
+    const int Nk = a.seqlens ? min(max(a.seqlens[b], 0), a.Nk) : a.Nk;
     const int k0 = s * a.chunk;
     const int k1 = min(Nk, k0 + a.chunk);
 
@@ -105,7 +107,7 @@ __global__ __launch_bounds__(64 * NW, 1) void decode_split_kernel(DecodeArgs a) 
     const S *kbase = reinterpret_cast<const S *>(a.k);
     const S *vbase = reinterpret_cast<const S *>(a.v);
     const size_t row_stride = (size_t)a.Hkv * D;                  // elements between keys
-    const size_t head_off = ((size_t)b * Nk * a.Hkv + g) * D;     // key 0 of (b, g)
+    const size_t head_off = ((size_t)b * a.Nk * a.Hkv + g) * D;   // key 0 of (b, g)
 
     unsigned short *kst = reinterpret_cast<unsigned short *>(smem) + w * SM::WAVE;
     unsigned short *vst = kst + KPW * SM::KS;
@@ -308,8 +310,9 @@ __global__ __launch_bounds__(D) void decode_combine_kernel(const float *__restri
         }
         M = Mc;
     }
-    reinterpret_cast<TOUT *>(o)[(size_t)bh * D + t] = from_f32<TOUT>(acc / L);
-    if (lse && t == 0) lse[bh] = (M + log2f(L)) * kLn2;
+    // a sequence with no valid key (per-sequence lengths) gives 0 and -inf
+    reinterpret_cast<TOUT *>(o)[(size_t)bh * D + t] = from_f32<TOUT>(L > 0.f ? acc / L : 0.f);
+    if (lse && t == 0) lse[bh] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
 }
 
 template <typename TIN, typename TOUT, int D>
@@ -328,6 +331,7 @@ hipError_t launch_t(const Problem &p, int S, void *ws, hipStream_t stream) {
     a.nqg = (G + QG - 1) / QG;
     a.c = __builtin_fabsf(p.scale) * kLog2e;
     a.qsign = p.scale < 0.f ? 0x80008000u : 0u;
+    a.seqlens = p.seqlens;
     const long long nblocks = (long long)p.B * p.Hkv * a.nqg * S;
     if (nblocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL((decode_split_kernel<TIN, D>), dim3((unsigned)nblocks), dim3(64 * NW), 0,

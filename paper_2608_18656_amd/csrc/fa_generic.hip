@@ -24,6 +24,7 @@ struct GenericArgs {
     int B, Hq, Hkv, Nq, Nk, D;
     float c;   // scale * log2(e), signed
     int nmb;   // row blocks of 64
+    const int *seqlens;   // valid keys per batch element (NULL: Nk for all)
 };
 
 template <typename T> struct Scalar { typedef T type; };
@@ -45,7 +46,9 @@ __global__ __launch_bounds__(256) void generic_kernel(GenericArgs a) {
     const int h = bid % a.Hq;
     const int b = bid / a.Hq;
     const int G = a.Hq / a.Hkv, g = h / G;
-    const int D = a.D, Nq = a.Nq, Nk = a.Nk;
+    const int D = a.D, Nq = a.Nq;
+    // valid keys of this batch element (a.Nk rows per element in K and V)
+    const int Nk = a.seqlens ? min(max(a.seqlens[b], 0), a.Nk) : a.Nk;
     const int qi = mb * 64 + row;
     const int off = Nk - Nq;
     const int last_blk = min(mb * 64 + 64, Nq) - 1;
@@ -90,7 +93,7 @@ __global__ __launch_bounds__(256) void generic_kernel(GenericArgs a) {
             kr[c] = float4_t{};
             vr[c] = float4_t{};
             if (kk < KT && key < Nk && d < D) {
-                const size_t o = ((size_t)((size_t)b * Nk + key) * a.Hkv + g) * D + d;
+                const size_t o = ((size_t)((size_t)b * a.Nk + key) * a.Hkv + g) * D + d;
                 kr[c] = load4(kb_ + o);
                 vr[c] = load4(vb_ + o);
             }
@@ -149,7 +152,7 @@ __global__ __launch_bounds__(256) void generic_kernel(GenericArgs a) {
         }
     }
     if (qi >= Nq) return;
-    const float inv = 1.f / lsum;
+    const float inv = lsum > 0.f ? 1.f / lsum : 0.f;   // no visible key: 0
     TOUT *op = reinterpret_cast<TOUT *>(a.o) + ((size_t)((size_t)b * Nq + qi) * a.Hq + h) * D;
 #pragma unroll
     for (int i = 0; i < NP; ++i) {
@@ -159,7 +162,8 @@ __global__ __launch_bounds__(256) void generic_kernel(GenericArgs a) {
             op[d + 1] = from_f32<TOUT>(o1[i] * inv);
         }
     }
-    if (a.lse && part == 0) a.lse[((size_t)b * a.Hq + h) * Nq + qi] = (m + log2f(lsum)) * kLn2;
+    if (a.lse && part == 0)
+        a.lse[((size_t)b * a.Hq + h) * Nq + qi] = lsum > 0.f ? (m + log2f(lsum)) * kLn2 : -INFINITY;
 }
 
 template <typename TIN, typename TOUT, int DMAX>
@@ -167,6 +171,7 @@ hipError_t launch_t(const Problem &p, hipStream_t stream) {
     GenericArgs a;
     a.q = p.q; a.k = p.k; a.v = p.v; a.o = p.o; a.lse = p.lse;
     a.B = p.B; a.Hq = p.Hq; a.Hkv = p.Hkv; a.Nq = p.Nq; a.Nk = p.Nk; a.D = p.D;
+    a.seqlens = p.seqlens;
     a.c = p.scale * kLog2e;
     a.nmb = (p.Nq + 63) / 64;
     const long long nblocks = (long long)a.nmb * p.B * p.Hq;

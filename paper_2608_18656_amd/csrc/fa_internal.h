@@ -18,6 +18,7 @@ struct Problem {
     float scale;
     fa_dtype_t in, out;
     int hw;   // prefill query heads per workgroup (0: the default choice)
+    const int *seqlens;   // device [B]: valid keys per batch element (NULL: Nk for all)
 };
 
 // Each launcher enqueues its kernels on `stream` and returns the first HIP

@@ -62,6 +62,7 @@ struct PrefillArgs {
     int nmb;          // row blocks of 32 * (4 / HW) rows
     int nhg;          // head groups per key/value head (G / HW)
     int pair;         // 1: every workgroup is resident at once; order heavy/light pairs
+    const int *seqlens;   // valid keys per batch element (NULL: Nk for all)
 };
 
 // Tile shape per head size.  Every wave handles 32 query rows and 32 keys of
@@ -126,8 +127,12 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
     const int row0_wg = mb * (WR * RB);
     const int row0 = row0_wg + rs * WR;
     const int qi = row0 + lq;
-    const int off = a.Nk - a.Nq;
-    const int Nq = a.Nq, Nk = a.Nk;
+    const int Nq = a.Nq;
+    // Valid keys of this batch element: with per-sequence lengths the K/V
+    // tensors hold a.Nk rows per batch element of which the first seqlens[b]
+    // are valid, and the queries are the sequence's last Nq positions.
+    const int Nk = a.seqlens ? min(max(a.seqlens[b], 0), a.Nk) : a.Nk;
+    const int off = Nk - Nq;
 
     // Key extents: workgroup, this slot, and keys every row of the slot sees.
     const int last_wg = min(row0_wg + WR * RB, Nq) - 1;
@@ -163,7 +168,7 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
     constexpr int KP = BC / 2;                  // key pairs per tile
     const bool kgroup = w < NT / 128;           // first half of the workgroup: K (wave-uniform)
     const S *kvbase = reinterpret_cast<const S *>(kgroup ? a.k : a.v) +
-                      ((size_t)b * Nk * a.Hkv + g) * D;
+                      ((size_t)b * a.Nk * a.Hkv + g) * D;
     const int st = kgroup ? tid : tid - NT / 2;
     const size_t row_elems = (size_t)a.Hkv * D;      // elements between consecutive keys
     // tile-relative key and column of load i of this thread
@@ -469,7 +474,9 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
         m_run = M;
     }
     const float l_tot = pair_sum(l_run);
-    const float inv = 1.f / l_tot;
+    // a row with no visible key (only with per-sequence lengths) gives 0 and
+    // a log-sum-exp of -inf
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
     if (qi < Nq) {
         TOUT *op = reinterpret_cast<TOUT *>(a.o) + ((size_t)((size_t)b * Nq + qi) * a.Hq + h) * D;
 #pragma unroll
@@ -491,7 +498,7 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
             }
         }
         if (a.lse && lh == 0)
-            a.lse[((size_t)b * a.Hq + h) * Nq + qi] = (m_run + log2f(l_tot)) * kLn2;
+            a.lse[((size_t)b * a.Hq + h) * Nq + qi] = l_tot > 0.f ? (m_run + log2f(l_tot)) * kLn2 : -INFINITY;
     }
 }
 
@@ -511,6 +518,7 @@ hipError_t launch_t(const Problem &p, hipStream_t stream) {
     PrefillArgs a;
     a.q = p.q; a.k = p.k; a.v = p.v; a.o = p.o; a.lse = p.lse;
     a.B = p.B; a.Hq = p.Hq; a.Hkv = p.Hkv; a.Nq = p.Nq; a.Nk = p.Nk;
+    a.seqlens = p.seqlens;
     // A zero scale keeps a tiny positive factor: every visible exponent is then
     // exactly 0 in fp32, and masked (-inf) scores still give 0.
     a.c = __builtin_fmaxf(__builtin_fabsf(p.scale), 1e-30f) * kLog2e;

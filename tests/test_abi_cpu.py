@@ -106,3 +106,15 @@ def test_packing_rejected_before_any_launch(packing, Hq, Hkv):
     st = lib.fa_fwd_packed(GOOD["q"], GOOD["k"], GOOD["v"], GOOD["o"], GOOD["lse"], 1, Hq, Hkv,
                            8, 8, 64, 1, 0.125, None, 0, 0, packing)
     assert st == 13
+
+
+def test_kvcache_sequence_lengths_checked_before_any_launch():
+    """fa_fwd_kvcache: NULL, misaligned or output-overlapping seqlens_k are
+    refused on the host (no HIP call)."""
+    lib = _lib.load()
+    def st(seqlens, o=GOOD["o"]):
+        return lib.fa_fwd_kvcache(GOOD["q"], GOOD["k"], GOOD["v"], o, GOOD["lse"], seqlens, 2, 4, 2,
+                                  8, 8, 64, 1, 0.125, None, 0, 0)
+    assert st(None) == 1
+    assert st(41 * A + 2) == 7
+    assert st(25 * A + 64) == 8          # inside o

@@ -261,3 +261,56 @@ def test_head_packing_schedules_agree_bitwise(name):
         assert torch.equal(o, ref_o) and torch.equal(lse, ref_l), f"packing {hw}"
     o_ref, l_ref = oracle_full(q, k, v, w.causal, w.softmax_scale)
     check_against(outs[1][0], outs[1][1], o_ref, l_ref, DTYPES[w.dtype], True, f"{name} per-head")
+
+
+def _kvcache_check(q, k, v, seqlens, causal, scale, dt, label):
+    """fa_fwd_kvcache against the oracle run on each sequence's valid cache
+    rows; query rows that see no key must give 0 and lse -inf."""
+    qd, kd, vd = (t.cuda() for t in (q, k, v))
+    sl = torch.tensor(seqlens, dtype=torch.int32, device="cuda")
+    o, lse = fa.fwd_kvcache(qd, kd, vd, sl, causal=causal, scale=scale, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    Nq = q.shape[1]
+    for b, L in enumerate(seqlens):
+        first = max(Nq - L, 0) if causal else (Nq if L == 0 else 0)   # first row with a key
+        if first > 0:
+            assert torch.all(o[b, :first] == 0), f"{label} b={b}: keyless rows not 0"
+            assert torch.all(torch.isneginf(lse[b, :, :first])), f"{label} b={b}: keyless lse"
+        if first < Nq:
+            o_ref, l_ref = oracle.attention(q[b:b + 1, first:].contiguous(), k[b:b + 1, :L].contiguous(),
+                                            v[b:b + 1, :L].contiguous(), causal, scale)
+            check_against(o[b:b + 1, first:].contiguous(), lse[b:b + 1, :, first:].contiguous(),
+                          o_ref, l_ref, DTYPES[dt], True, f"{label} b={b} L={L}")
+    return o, lse
+
+
+@pytest.mark.parametrize("case", [
+    # decode against caches of different fill, including an empty one
+    (4, 32, 8, 1, 3000, 128, "bf16", False, [3000, 1, 1777, 0]),
+    (3, 16, 1, 1, 2500, 64, "f16", True, [2500, 33, 1024]),
+    # chunked prefill: Nq new tokens at the end of each sequence
+    (3, 8, 2, 70, 600, 64, "f16", True, [600, 70, 333]),
+    (2, 32, 8, 64, 512, 128, "bf16", True, [512, 200]),
+    # a chunk longer than its sequence: the first rows see no key
+    (2, 4, 4, 100, 256, 128, "bf16", True, [40, 256]),
+    # the vector-ALU kernel (fp32)
+    (2, 2, 2, 20, 150, 64, "f32", False, [150, 17]),
+], ids=lambda c: f"B{c[0]}Hq{c[1]}Hkv{c[2]}Nq{c[3]}Nk{c[4]}D{c[5]}{c[6]}{'c' if c[7] else ''}")
+def test_kvcache_per_sequence_lengths(case):
+    B, Hq, Hkv, Nq, Nk, D, dt, causal, seqlens = case
+    q, k, v = make_qkv(B, Hq, Hkv, Nq, Nk, D, dt, seed=900 + B * Nq)
+    _kvcache_check(q, k, v, seqlens, causal, default_scale(D), dt, "kvcache")
+
+
+@pytest.mark.parametrize("shape", [(2, 32, 8, 1, 2000, 128, "bf16", False),
+                                   (1, 32, 8, 333, 333, 64, "bf16", True),
+                                   (1, 16, 1, 200, 260, 64, "f16", True)])
+def test_kvcache_full_lengths_equal_fa_fwd_bitwise(shape):
+    B, Hq, Hkv, Nq, Nk, D, dt, causal = shape
+    q, k, v = make_qkv(B, Hq, Hkv, Nq, Nk, D, dt, seed=950 + Nq)
+    qd, kd, vd = (t.cuda() for t in (q, k, v))
+    sl = torch.full((B,), Nk, dtype=torch.int32, device="cuda")
+    o1, l1 = fa.fwd(qd, kd, vd, causal=causal, out_dtype=torch.float32)
+    o2, l2 = fa.fwd_kvcache(qd, kd, vd, sl, causal=causal, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
