@@ -137,6 +137,8 @@ def main():
     ap.add_argument("--workload", default="gqa_prefill_bf16")
     ap.add_argument("--no-extras", action="store_true", help="headline workload only")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-ablation", action="store_true",
+                    help="skip the inter-head packing ablation (e.g. under a kernel trace)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -226,7 +228,8 @@ def main():
         # inter-head packing ablation: the default schedule (the G query heads
         # of a K/V group share each staged K/V tile) against the per-head one
         ablation = []
-        for name in ("gqa_prefill_bf16", "gqa_prefill_d128_f16", "mqa_prefill_f16"):
+        for name in (() if args.no_ablation else
+                     ("gqa_prefill_bf16", "gqa_prefill_d128_f16", "mqa_prefill_f16")):
             x = WORKLOADS[name]
             steps = max(5, min(args.steps, 20))
             row = {"workload": name}
@@ -239,7 +242,8 @@ def main():
             ablation.append(row)
             log(f"[bench] packing {name}: packed {row['packed_us']} us, per-head "
                 f"{row['per_head_us']} us ({row['speedup']}x)")
-        result["packing_ablation"] = ablation
+        if ablation:
+            result["packing_ablation"] = ablation
         # achievable HBM bandwidth for context: a plain 1 GiB device copy
         src = torch.empty(1 << 29, dtype=torch.float16, device="cuda").fill_(1.0)
         dst = torch.empty_like(src)
