@@ -155,8 +155,8 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
         }
     }
 
-    // Tile staging.  The first half of the workgroup copies K rows (chunk
-    // c = st + (NT / 2) i: key c / CPR, 16-byte column chunk c % CPR); the second
+    // Tile staging.  The second half of the workgroup copies K rows (chunk
+    // c = st + (NT / 2) i: key c / CPR, 16-byte column chunk c % CPR); the first
     // half stages V transposed: unit u holds keys 2p, 2p+1 (p = u % KP) of
     // column chunk u / KP and writes eight 32-bit words, each the (2p, 2p+1)
     // pair of one column d, into row d of V^T (as fp16).  Within every 16 keys
@@ -166,10 +166,13 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
     // byte offset, so a step spends no vector instructions on addresses.
     constexpr int SL = BC * D / (4 * NT);       // 16-byte loads per thread per tile
     constexpr int KP = BC / 2;                  // key pairs per tile
-    const bool kgroup = w < NT / 128;           // first half of the workgroup: K (wave-uniform)
+    // second half of the workgroup: K (wave-uniform).  The older wave of each
+    // SIMD wins issue priority and finishes its softmax first, so it takes the
+    // heavier V staging (the bf16 conversion) and the later one the K copy.
+    const bool kgroup = w >= NT / 128;
     const S *kvbase = reinterpret_cast<const S *>(kgroup ? a.k : a.v) +
                       ((size_t)b * a.Nk * a.Hkv + g) * D;
-    const int st = kgroup ? tid : tid - NT / 2;
+    const int st = kgroup ? tid - NT / 2 : tid;
     const size_t row_elems = (size_t)a.Hkv * D;      // elements between consecutive keys
     // tile-relative key and column of load i of this thread
     auto lkey = [&](int i) {
