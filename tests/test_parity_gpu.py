@@ -7,7 +7,10 @@ two decode workloads at full size with every output compared; the three
 prefill workloads at full size on sampled rows; edge shapes (Nk = 1, ragged
 tiles, causal with Nq < Nk, group sizes 1 to 32, odd group sizes, negative
 and zero scale, the vector-ALU path for fp32 and other head dimensions);
-forced split counts including empty splits; determinism; error reporting.
+forced split counts including empty splits; determinism; error reporting;
+a caller-owned decode workspace; the prefill query-head packings (bitwise
+agreement); K/V caches with per-sequence lengths (decode, chunked prefill,
+rows with no visible key); tensors of more than 2^31 elements.
 """
 import zlib
 
@@ -314,3 +317,28 @@ def test_kvcache_full_lengths_equal_fa_fwd_bitwise(shape):
     o2, l2 = fa.fwd_kvcache(qd, kd, vd, sl, causal=causal, out_dtype=torch.float32)
     torch.cuda.synchronize()
     assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+@pytest.mark.parametrize("Nq,causal", [(1, False), (64, False), (64, True)],
+                         ids=["decode", "prefill", "prefill_causal"])
+def test_offsets_beyond_2_31_elements(Nq, causal):
+    """K and V of 2 x 2^31 elements (about 8.6 GB each): batch element 1
+    starts past 2^31, so any 32-bit index arithmetic would wrap.  Its output
+    must equal, bit for bit, a call on that element alone (whose indices are
+    small; the decode call gets a fixed split count, since the default one
+    depends on B)."""
+    B, Hq, Hkv, Nk, D = 2, 32, 8, 1 << 21, 128
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(2024)
+    k = torch.randn((B, Nk, Hkv, D), generator=gen, device="cuda", dtype=torch.float32).to(torch.bfloat16)
+    v = torch.randn((B, Nk, Hkv, D), generator=gen, device="cuda", dtype=torch.float32).to(torch.bfloat16)
+    q = torch.randn((B, Nq, Hq, D), generator=gen, device="cuda", dtype=torch.float32).to(torch.bfloat16)
+    assert k[1].numel() >= 1 << 31
+    S = 16 if Nq == 1 else None   # the same decode split count for both calls
+    o, lse = fa.fwd(q, k, v, causal=causal, out_dtype=torch.float32, num_splits=S)
+    o1, lse1 = fa.fwd(q[1:2], k[1:2], v[1:2], causal=causal, out_dtype=torch.float32, num_splits=S)
+    torch.cuda.synchronize()
+    assert torch.isfinite(o).all()
+    assert torch.equal(o[1:2], o1) and torch.equal(lse[1:2], lse1)
+    del k, v
+    torch.cuda.empty_cache()
