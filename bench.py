@@ -9,7 +9,9 @@ plus log-sum-exp merge) is timed in the same run on the GQA decode workload
 (B=16, Hq=32, Hkv=8, Nk=8192, D=128, bf16) as KV-read GB/s, and the other
 workloads are reported alongside.  The fp64 CPU oracle is timed on the host
 cores on the headline workload as a baseline (not a target), and the GPU
-output of the benchmark is checked against it.
+output of the benchmark is checked against it.  The Q8_0 matrix-vector
+products of a decode step (the linear layers of a TinyLlama-1.1B shaped
+model) are reported under "q8_0_gemv" as weight GB/s.
 
 Prints ONE JSON line on stdout; progress goes to stderr.
 """
@@ -129,6 +131,117 @@ def cpu_baseline(w, q_cpu_dev, o_dev, lse_dev):
             {"max_abs_err_vs_oracle": err, "lse_max_abs_err": lerr})
 
 
+def q8_decode_step(torch, fa, steps, warmup, with_cpu):
+    """The Q8_0 matrix-vector products of one decode step of a TinyLlama-1.1B
+    shaped model (22 layers; per layer the fused q/k/v projection, the output
+    projection, the fused gate/up projection and the down projection, each
+    with its own weights, 1.03 GB in all), launched in order on one stream and
+    replayed from a HIP graph; the value is weight GB/s (34 bytes per 32
+    weights, read once).  Also the average time of each launch shape, and one
+    launch over 22 stacked gate/up matrices (539 MB) as the streaming rate."""
+    from paper_2608_18656_amd.inputs import Q8_LAYER_SHAPES, Q8_LAYERS, make_q8_0
+
+    base = [make_q8_0(M, K, seed=2000 + i, x_dtype="bf16") for i, (_, M, K) in enumerate(Q8_LAYER_SHAPES)]
+    W = [[b[0].cuda() for b in base]]
+    for _ in range(1, Q8_LAYERS):
+        W.append([t.clone() for t in W[0]])
+    X = [b[1].cuda() for b in base]
+    Y = [torch.empty(M, dtype=torch.bfloat16, device="cuda") for _, M, _ in Q8_LAYER_SHAPES]
+    total = sum(t.numel() for layer in W for t in layer)
+
+    def launch(l, i):
+        fa.q8_0_gemv(W[l][i], X[i], out=Y[i])
+
+    def graph_of(calls):
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            for c in calls:
+                c()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            for c in calls:
+                c()
+        return g
+
+    def time_graph(g, n):
+        for _ in range(warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for _ in range(n):
+            g.replay()
+        t1.record()
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) / n
+
+    # eager reference of the last layer's outputs, then the graph, replayed
+    # several times and checked bitwise against it
+    for i in range(len(Q8_LAYER_SHAPES)):
+        launch(Q8_LAYERS - 1, i)
+    torch.cuda.synchronize()
+    eager = [y.clone() for y in Y]
+    step = graph_of([(lambda l=l, i=i: launch(l, i)) for l in range(Q8_LAYERS)
+                     for i in range(len(Q8_LAYER_SHAPES))])
+    for _ in range(3):
+        step.replay()
+        torch.cuda.synchronize()
+        if not all(torch.equal(a, b) for a, b in zip(eager, Y)):
+            raise RuntimeError("graph replay of the Q8_0 products differs from the eager result")
+    ms = time_graph(step, steps)
+    gbs = total / (ms * 1e-3) / 1e9
+    per_shape = []
+    for i, (name, M, K) in enumerate(Q8_LAYER_SHAPES):
+        g = graph_of([(lambda l=l, i=i: launch(l, i)) for l in range(Q8_LAYERS)])
+        sms = time_graph(g, steps) / Q8_LAYERS
+        nbytes = W[0][i].numel()
+        per_shape.append({"name": name, "M": M, "K": K, "bytes": nbytes, "us": round(sms * 1e3, 2),
+                          "GB_s": round(nbytes / (sms * 1e-3) / 1e9, 1)})
+        del g
+    dom = max(per_shape, key=lambda r: r["bytes"])   # the largest launch dominates the step
+    # one large launch: the gate/up matrices of all layers stacked
+    Mbig, Kbig = Q8_LAYER_SHAPES[2][1] * Q8_LAYERS, Q8_LAYER_SHAPES[2][2]
+    wbig = torch.cat([W[l][2] for l in range(Q8_LAYERS)], dim=0)
+    ybig = torch.empty(Mbig, dtype=torch.bfloat16, device="cuda")
+    bms = time_calls(torch, [lambda: fa.q8_0_gemv(wbig, X[2], out=ybig)], max(5, steps // 2), 2)
+    out = {
+        "workload": "tinyllama-1.1b-shaped Q8_0 decode linear layers (22 layers x "
+                    "{qkv 2560x2048, o 2048x2048, gate_up 11264x2048, down 2048x5632}), bf16 x",
+        "metric": "weight GB/s (Q8_0 bytes read once per step)",
+        "us_per_step": round(ms * 1e3, 1), "bytes_per_step": total,
+        "value": round(gbs, 1), "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+        "launches_per_step": Q8_LAYERS * len(Q8_LAYER_SHAPES), "graph": True,
+        "per_shape": per_shape,
+        "roofline": {"bound": "hbm", "kernel": "q8_gemv_kernel (" + dom["name"] + ")",
+                     "achieved": dom["GB_s"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(dom["GB_s"] / PEAK_HBM_GBS, 4),
+                     "algorithmic_per_launch": dom["bytes"]},
+        "streaming": {"M": Mbig, "K": Kbig, "bytes": wbig.numel(), "us": round(bms * 1e3, 1),
+                      "GB_s": round(wbig.numel() / (bms * 1e-3) / 1e9, 1),
+                      "frac": round(wbig.numel() / (bms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
+    }
+    log(f"[bench] q8_0 decode step: {ms * 1e3:.1f} us, {gbs:.0f} GB/s ({100 * gbs / PEAK_HBM_GBS:.1f}%); "
+        f"streaming {out['streaming']['GB_s']} GB/s")
+    if with_cpu:
+        from oracle import q8 as oracle_q8
+
+        wc = [b[0].numpy() for b in base]
+        xc = [b[1].float().numpy() for b in base]
+        t0 = time.perf_counter()
+        for wi, xi in zip(wc, xc):
+            oracle_q8.gemv(wi, xi)
+        wall = time.perf_counter() - t0
+        nbytes = sum(wi.size for wi in wc)
+        out["cpu_baseline"] = {"value": round(nbytes / wall / 1e9, 3), "unit": "GB/s", "cores": 1,
+                               "kind": "oracle",
+                               "sample": "one layer's four matrices (46.8 MB), fp64 C, one thread"}
+    del W, wbig
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -244,6 +357,8 @@ def main():
                 f"{row['per_head_us']} us ({row['speedup']}x)")
         if ablation:
             result["packing_ablation"] = ablation
+        result["q8_0_gemv"] = q8_decode_step(torch, fa, max(5, min(args.steps, 20)), 3,
+                                             not args.no_cpu_baseline)
         # achievable HBM bandwidth for context: a plain 1 GiB device copy
         src = torch.empty(1 << 29, dtype=torch.float16, device="cuda").fill_(1.0)
         dst = torch.empty_like(src)

@@ -178,6 +178,30 @@ fa_status_t fa_release_workspace(void);
  * misaligned pointer, FA_ERR_HIP when the current device cannot be read. */
 fa_status_t fa_set_workspace(void *dev_ptr, size_t bytes);
 
+/* Q8_0 matrix-vector product y = W x, the form the linear projection and
+ * feed-forward layers take in decode, where a single token is processed
+ * (Sec. 4.3).  W (M x K, row-major) is in the 8-bit block format Q8_0 of
+ * Sec. 4.3 and Sec. 7: each row is K / 32 consecutive 34-byte blocks, a block
+ * being one IEEE binary16 scale d (bytes 0-1, little-endian) followed by 32
+ * signed 8-bit values q_0 .. q_31 (bytes 2-33), weight j of the block being
+ * d * q_j (symmetric, no zero point).  The scale comes first as Sec. 7 lays
+ * the block out (Sec. 4.3 places it after the values).
+ *   w  device, M * (K / 32) * 34 bytes, 4-byte aligned          read only
+ *   x  device, K elements of x_dtype (FA_F16, FA_BF16 or FA_F32),
+ *      16-byte aligned; used as given (not quantized)            read only
+ *   y  device, M elements of y_dtype (x_dtype or FA_F32)        written
+ * y[m] = sum over blocks b of d[m][b] * (sum_j q[m][b][j] * x[32 b + j]),
+ * accumulated in fp32 (products of the exact int8 values and fp32 x, one
+ * rounding per multiply-add), then rounded to nearest even in y_dtype.
+ * Non-finite scales give non-finite results whose sign and NaN-ness may
+ * differ from the term-by-term sum.  Enqueued on `stream`; allocates nothing.
+ * Errors (before any HIP call): FA_ERR_NULL for a NULL pointer, FA_ERR_DIM
+ * for M < 1, K < 32, K > 2^30 or K not a multiple of 32, FA_ERR_DTYPE for another dtype
+ * pair, FA_ERR_ALIGN for a misaligned pointer, FA_ERR_ALIAS when y overlaps w
+ * or x, FA_ERR_HIP when the launch fails. */
+fa_status_t fa_q8_0_gemv(const void *w, const void *x, void *y, int M, int K, fa_dtype_t x_dtype,
+                         fa_dtype_t y_dtype, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -8,7 +8,7 @@ from __future__ import annotations
 
 import math
 
-__all__ = ["fwd", "fwd_splitkv", "fwd_kvcache", "FaError", "validate", "workspace_bytes", "release_workspace",
+__all__ = ["fwd", "fwd_splitkv", "fwd_kvcache", "q8_0_gemv", "FaError", "validate", "workspace_bytes", "release_workspace",
            "set_workspace", "version", "DTYPE_CODES"]
 
 
@@ -136,6 +136,42 @@ def fwd_kvcache(q, k_cache, v_cache, seqlens_k, causal: bool = False, scale: flo
                                 codes[q.dtype], codes.get(odt, -1))
     _check(lib, st)
     return out, lse
+
+
+def q8_0_gemv(w, x, out=None, out_dtype=None):
+    """Q8_0 matrix-vector product y = W x (the decode-time linear layers).
+
+    ``w``: uint8 GPU tensor holding M rows of K / 32 Q8_0 blocks of 34 bytes
+    (binary16 scale, little-endian, then 32 int8 values), shaped [M, K/32, 34]
+    or [M, K/32 * 34], contiguous.  ``x``: [K] float16, bfloat16 or float32 on
+    the same device.  Returns y [M] in ``out_dtype`` (x's dtype, or float32).
+    See fa_q8_0_gemv in include/fa.h."""
+    from . import _lib
+
+    lib = _lib.load()
+    torch = _torch()
+    if not (w.is_cuda and x.is_cuda) or w.device != x.device:
+        raise ValueError("w and x must be GPU tensors on one device")
+    if w.dtype != torch.uint8 or not w.is_contiguous() or w.dim() not in (2, 3):
+        raise ValueError("w must be a contiguous uint8 [M, K/32, 34] or [M, K/32*34] tensor")
+    if x.dim() != 1 or not x.is_contiguous() or x.dtype not in _codes():
+        raise ValueError("x must be a contiguous 1-D float16, bfloat16 or float32 tensor")
+    M, K = w.shape[0], x.shape[0]
+    row_bytes = w[0].numel() if M > 0 else 0
+    if (w.dim() == 3 and w.shape[2] != 34) or K % 32 != 0 or row_bytes != K // 32 * 34:
+        raise ValueError("w must hold K/32 blocks of 34 bytes per row, K = len(x) a multiple of 32")
+    odt = x.dtype if out_dtype is None else out_dtype
+    if out is None:
+        out = torch.empty((M,), dtype=odt, device=x.device)
+    elif tuple(out.shape) != (M,) or out.dtype != odt or not out.is_contiguous() or out.device != x.device:
+        raise ValueError("out must be a contiguous [M] tensor of the output dtype")
+    codes = _codes()
+    stream = torch.cuda.current_stream(x.device).cuda_stream
+    with torch.cuda.device(x.device):
+        st = lib.fa_q8_0_gemv(w.data_ptr(), x.data_ptr(), out.data_ptr(), M, K, codes[x.dtype],
+                              codes.get(odt, -1), stream)
+    _check(lib, st)
+    return out
 
 
 def fwd_splitkv(q, k, v, num_splits: int, **kw):

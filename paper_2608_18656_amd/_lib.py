@@ -25,7 +25,8 @@ STATUS_NAMES = {
 # Every symbol include/fa.h declares.
 EXPORTS = ("fa_status_string", "fa_version", "fa_validate", "fa_fwd_f16", "fa_fwd_bf16",
            "fa_fwd_f32", "fa_fwd", "fa_fwd_splitkv", "fa_workspace_bytes",
-           "fa_release_workspace", "fa_set_workspace", "fa_fwd_packed", "fa_fwd_kvcache")
+           "fa_release_workspace", "fa_set_workspace", "fa_fwd_packed", "fa_fwd_kvcache",
+           "fa_q8_0_gemv")
 
 _lib = None
 
@@ -69,5 +70,7 @@ def load():
     lib.fa_release_workspace.restype = _I
     lib.fa_set_workspace.argtypes = [_P, ctypes.c_size_t]
     lib.fa_set_workspace.restype = _I
+    lib.fa_q8_0_gemv.argtypes = [_P, _P, _P, _I, _I, _I, _I, _P]
+    lib.fa_q8_0_gemv.restype = _I
     _lib = lib
     return lib

@@ -240,6 +240,24 @@ fa_status_t fa_set_workspace(void *dev_ptr, size_t bytes) {
     return FA_OK;
 }
 
+fa_status_t fa_q8_0_gemv(const void *w, const void *x, void *y, int M, int K, fa_dtype_t x_dtype,
+                         fa_dtype_t y_dtype, void *stream) {
+    if (!w || !x || !y) return FA_ERR_NULL;
+    if (M < 1 || K < 32 || K % 32 != 0 || K > (1 << 30)) return FA_ERR_DIM;
+    const bool xt_ok = x_dtype == FA_F16 || x_dtype == FA_BF16 || x_dtype == FA_F32;
+    if (!xt_ok || !(y_dtype == x_dtype || y_dtype == FA_F32)) return FA_ERR_DTYPE;
+    const size_t xe = esize(x_dtype), ye = esize(y_dtype);
+    if ((reinterpret_cast<uintptr_t>(w) & 3) || (reinterpret_cast<uintptr_t>(x) & 15) ||
+        (reinterpret_cast<uintptr_t>(y) & (ye - 1)))
+        return FA_ERR_ALIGN;
+    const size_t wb = (size_t)M * (size_t)(K / 32) * 34;
+    if (overlaps(y, (size_t)M * ye, w, wb) || overlaps(y, (size_t)M * ye, x, (size_t)K * xe))
+        return FA_ERR_ALIAS;
+    const hipError_t e =
+        fa::launch_q8_gemv(w, x, y, M, K, x_dtype, y_dtype, reinterpret_cast<hipStream_t>(stream));
+    return e == hipSuccess ? FA_OK : FA_ERR_HIP;
+}
+
 fa_status_t fa_release_workspace(void) {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return FA_ERR_HIP;

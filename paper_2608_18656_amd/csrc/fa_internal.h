@@ -26,6 +26,8 @@ struct Problem {
 hipError_t launch_prefill(const Problem &p, hipStream_t stream);
 hipError_t launch_generic(const Problem &p, hipStream_t stream);
 hipError_t launch_decode(const Problem &p, int splits, void *workspace, hipStream_t stream);
+hipError_t launch_q8_gemv(const void *w, const void *x, void *y, int M, int K, fa_dtype_t x_dtype,
+                          fa_dtype_t y_dtype, hipStream_t stream);
 
 // Decode split planning (shared by the dispatcher and fa_workspace_bytes).
 bool decode_supported(int Nq, int D, fa_dtype_t in);

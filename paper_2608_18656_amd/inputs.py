@@ -107,3 +107,52 @@ def shrink(w: Workload, **over) -> Workload:
     d = {f: getattr(w, f) for f in w.__dataclass_fields__}
     d.update(over)
     return Workload(**d)
+
+
+# Q8_0 weights for the decode-time linear layers.  Shapes of the TinyLlama-1.1B
+# projections the paper runs with Q8_0 weights (Table 3: 32 query heads and
+# 4 key/value heads of 64; hidden size 2048, feed-forward size 5632, 22
+# layers), with the projections that share an input stored as one matrix:
+# (name, M rows, K columns).
+Q8_LAYER_SHAPES = (
+    ("qkv", 2048 + 2 * 256, 2048),
+    ("o", 2048, 2048),
+    ("gate_up", 2 * 5632, 2048),
+    ("down", 2048, 5632),
+)
+Q8_LAYERS = 22
+
+
+def make_q8_0(M: int, K: int, seed: int, x_dtype: str = "bf16"):
+    """Seeded Q8_0 weights and activations on the CPU.
+
+    Returns (w, x): w uint8 [M, K/32, 34], each block a binary16 scale (bytes
+    0-1, little-endian) then 32 int8 values; x [K] in ``x_dtype``.  Values are
+    drawn directly in the stored form (no quantisation step): the int8 values
+    are N(0, 40^2) rounded and clipped to [-127, 127] with one entry per block
+    set to +-127 (a block quantised from its largest magnitude has one), the
+    scales |N(0, 1)| * 2e-4 + 1e-4 rounded to binary16 (weights of standard
+    deviation about 0.02), and x N(0, 1) rounded to ``x_dtype``."""
+    if K % 32 != 0 or K < 32 or M < 1:
+        raise ValueError("need M >= 1 and K a positive multiple of 32")
+    nb = K // 32
+    gen = torch.Generator(device="cpu")
+    gen.manual_seed(int(seed))
+    q = torch.randn((M, nb, 32), generator=gen, dtype=torch.float32).mul_(40.0).round_()
+    q.clamp_(-127.0, 127.0)
+    pos = torch.randint(0, 32, (M, nb, 1), generator=gen)
+    sgn = torch.randint(0, 2, (M, nb, 1), generator=gen).to(torch.float32).mul_(254.0).sub_(127.0)
+    q.scatter_(2, pos, sgn)
+    d = torch.randn((M, nb), generator=gen, dtype=torch.float32).abs_().mul_(2e-4).add_(1e-4)
+    x = torch.randn((K,), generator=gen, dtype=torch.float32)
+    return pack_q8_0(d.to(torch.float16), q.to(torch.int8)), x.to(DTYPES[x_dtype])
+
+
+def pack_q8_0(d: torch.Tensor, q: torch.Tensor) -> torch.Tensor:
+    """Byte layout of Q8_0 rows: d float16 [M, nb] and q int8 [M, nb, 32] ->
+    uint8 [M, nb, 34] (scale bytes first, little-endian, then the 32 values)."""
+    M, nb = d.shape
+    w = torch.empty((M, nb, 34), dtype=torch.uint8)
+    w[:, :, 0:2] = d.contiguous().view(torch.uint8).reshape(M, nb, 2)
+    w[:, :, 2:] = q.contiguous().view(torch.uint8)
+    return w

@@ -118,3 +118,25 @@ def test_kvcache_sequence_lengths_checked_before_any_launch():
     assert st(None) == 1
     assert st(41 * A + 2) == 7
     assert st(25 * A + 64) == 8          # inside o
+
+
+def test_q8_gemv_argument_errors_before_any_launch():
+    """fa_q8_0_gemv's checks return before any HIP call (fake addresses)."""
+    lib = _lib.load()
+    W, X, Y = 1 << 20, 64 << 20, 96 << 20
+    F16, BF16, F32 = _lib.FA_F16, _lib.FA_BF16, _lib.FA_F32
+
+    def call(w=W, x=X, y=Y, M=8, K=64, xt=BF16, yt=BF16):
+        return lib.fa_q8_0_gemv(w, x, y, M, K, xt, yt, None)
+
+    assert call(w=None) == 1 and call(x=None) == 1 and call(y=None) == 1
+    for M, K in [(0, 64), (-1, 64), (8, 0), (8, 16), (8, 48), (8, 33), (1, (1 << 30) + 32)]:
+        assert call(M=M, K=K) == 2, (M, K)
+    assert call(xt=3) == 9 and call(xt=F16, yt=BF16) == 9 and call(xt=F32, yt=F16) == 9
+    assert call(yt=7) == 9
+    assert call(w=W + 2) == 7                      # weights need 4-byte alignment
+    assert call(x=X + 2) == 7 and call(x=X + 8) == 7   # x needs 16-byte alignment
+    assert call(y=Y + 1) == 7 and call(xt=F32, yt=F32, y=Y + 2) == 7
+    assert call(y=W + 100) == 8                    # y inside w (8 * 2 * 34 bytes)
+    assert call(y=X + 64) == 8                     # y inside x
+    assert call(y=W + 8 * 2 * 34) != 8             # y right after w: no overlap reported
