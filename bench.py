@@ -35,6 +35,7 @@ PREFILL_SOURCES = ["paper_2608_18656_amd/csrc/fa_prefill.hip",
                    "paper_2608_18656_amd/csrc/fa_common.h"]
 DECODE_SOURCES = ["paper_2608_18656_amd/csrc/fa_decode.hip",
                   "paper_2608_18656_amd/csrc/fa_common.h"]
+Q8_SOURCES = ["paper_2608_18656_amd/csrc/fa_q8.hip"]
 
 
 def log(*a):
@@ -217,6 +218,7 @@ def q8_decode_step(torch, fa, steps, warmup, with_cpu):
         "roofline": {"bound": "hbm", "kernel": "q8_gemv_kernel (" + dom["name"] + ")",
                      "achieved": dom["GB_s"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(dom["GB_s"] / PEAK_HBM_GBS, 4),
+                     "traffic": stored_traffic("q8_gemv_kernel", dom["name"], Q8_SOURCES),
                      "algorithmic_per_launch": dom["bytes"]},
         "streaming": {"M": Mbig, "K": Kbig, "bytes": wbig.numel(), "us": round(bms * 1e3, 1),
                       "GB_s": round(wbig.numel() / (bms * 1e-3) / 1e9, 1),

@@ -4,6 +4,10 @@ HBM byte counters).
 
     python3 paper_2608_18656_amd/profile_run.py gqa_prefill_bf16 5
     python3 paper_2608_18656_amd/profile_run.py copy 268435456 5
+    python3 paper_2608_18656_amd/profile_run.py q8_gate_up 5
+
+``q8_<name>`` runs the Q8_0 matrix-vector product of one TinyLlama-shaped
+projection (qkv, o, gate_up or down; bf16 activations).
 """
 from __future__ import annotations
 
@@ -28,9 +32,18 @@ def main(argv):
         print(f"copied {nbytes} bytes x {reps}", flush=True)
         return
     import paper_2608_18656_amd as fa
-    from paper_2608_18656_amd.inputs import WORKLOADS, make_workload
+    from paper_2608_18656_amd.inputs import Q8_LAYER_SHAPES, WORKLOADS, make_q8_0, make_workload
 
     reps = int(argv[2]) if len(argv) > 2 else 5
+    if what.startswith("q8_"):
+        shape = {n: (M, K) for n, M, K in Q8_LAYER_SHAPES}[what[3:]]
+        w, x = make_q8_0(*shape, seed=2000, x_dtype="bf16")
+        w, x = w.cuda(), x.cuda()
+        for _ in range(reps):
+            fa.q8_0_gemv(w, x)
+        torch.cuda.synchronize()
+        print(f"ran {what} {shape} x {reps}", flush=True)
+        return
     w = WORKLOADS[what]
     q, k, v = (t.cuda() for t in make_workload(w))
     for _ in range(reps):
