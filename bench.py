@@ -132,6 +132,38 @@ def cpu_baseline(w, q_cpu_dev, o_dev, lse_dev):
             {"max_abs_err_vs_oracle": err, "lse_max_abs_err": lerr})
 
 
+def paged_decode(torch, fa, w, steps, warmup, page_size):
+    """Decode of workload ``w`` against a paged cache: the K/V rows of each
+    sequence scattered over pages of ``page_size`` keys in a seeded random
+    order (two pools alternated, so that every call streams from HBM); every
+    sequence full.  Returns us per call and K+V GB/s."""
+    from paper_2608_18656_amd.inputs import make_workload
+
+    q, k, v = make_workload(w)
+    max_pages = w.Nk // page_size
+    npg = w.B * max_pages
+    sets = []
+    for r in range(2):
+        gen = torch.Generator().manual_seed(4000 + r)
+        perm = torch.randperm(npg, generator=gen)
+        table = perm.reshape(w.B, max_pages).to(torch.int32)
+        kp = torch.empty((npg, page_size, w.Hkv, w.D), dtype=k.dtype)
+        vp = torch.empty_like(kp)
+        kp[perm] = k.reshape(npg, page_size, w.Hkv, w.D)
+        vp[perm] = v.reshape(npg, page_size, w.Hkv, w.D)
+        sets.append((kp.cuda(), vp.cuda(), table.cuda()))
+    qd = q.cuda()
+    sl = torch.full((w.B,), w.Nk, dtype=torch.int32, device="cuda")
+    out = torch.empty_like(qd)
+    lse = torch.empty((w.B, w.Hq, 1), dtype=torch.float32, device="cuda")
+    fns = [(lambda s=s: fa.fwd_kvcache_paged(qd, s[0], s[1], s[2], sl, scale=w.softmax_scale, out=out,
+                                             lse=lse)) for s in sets]
+    ms = time_calls(torch, fns, steps, warmup)
+    del sets
+    torch.cuda.empty_cache()
+    return ms * 1e3, w.kv_bytes() / (ms * 1e-3) / 1e9
+
+
 def q8_decode_step(torch, fa, steps, warmup, with_cpu):
     """The Q8_0 matrix-vector products of one decode step of a TinyLlama-1.1B
     shaped model (22 layers; per layer the fused q/k/v projection, the output
@@ -359,6 +391,15 @@ def main():
                 f"{row['per_head_us']} us ({row['speedup']}x)")
         if ablation:
             result["packing_ablation"] = ablation
+        # decode against a paged K/V cache (pages of 64 and 256 keys, shuffled)
+        xw = WORKLOADS["gqa_decode_bf16"]
+        paged = {"workload": xw.name, "metric": "decode KV GB/s, K/V in shuffled pages", "pages": []}
+        for ps in (64, 256):
+            pus, pgbs = paged_decode(torch, fa, xw, max(5, min(args.steps, 30)), 3, ps)
+            paged["pages"].append({"page_size": ps, "us_per_call": round(pus, 2), "value": round(pgbs, 1),
+                                   "unit": "GB/s", "frac": round(pgbs / PEAK_HBM_GBS, 4)})
+            log(f"[bench] paged decode, pages of {ps}: {pus:.1f} us/call, {pgbs:.0f} GB/s")
+        result["paged_decode"] = paged
         result["q8_0_gemv"] = q8_decode_step(torch, fa, max(5, min(args.steps, 20)), 3,
                                              not args.no_cpu_baseline)
         # achievable HBM bandwidth for context: a plain 1 GiB device copy

@@ -153,6 +153,35 @@ fa_status_t fa_fwd_kvcache(const void *q, const void *k, const void *v, void *o,
                            int causal, float scale, void *stream, fa_dtype_t in_dtype,
                            fa_dtype_t out_dtype);
 
+/* Attention against a paged key/value cache (decode, and chunked prefill of
+ * Nq new tokens), the cache layout of serving systems: keys and values live
+ * in a pool of fixed-size pages,
+ *   k_pages, v_pages  [num_pages][page_size][Hkv][D]   element type = in_dtype, read only
+ *   block_table       [B][max_pages] int32 (device): page of each block of
+ *                     page_size keys of each sequence; key j of batch element
+ *                     b is row j % page_size of page block_table[b][j / page_size]
+ *   seqlens_k         [B] int32 (device): valid keys of each sequence
+ * and otherwise the semantics of fa_fwd_kvcache with Nk = page_size *
+ * max_pages (lengths clamped to [0, Nk], the Nq queries are each sequence's
+ * last positions, bottom-right causal alignment per sequence, rows that see no
+ * key give 0 and -inf).  Only table entries for blocks that hold valid keys
+ * are read; an entry outside [0, num_pages) is clamped into that range (a
+ * wrong table gives wrong results, never an access outside the pool).  With
+ * every sequence's pages laid out in order the result equals fa_fwd_kvcache's
+ * on the gathered cache bit for bit.  fp16 / bf16 with D in {64, 128} only.
+ * Decode calls (Nq = 1) use the decode workspace of fa_workspace_bytes(B, Hq,
+ * Hkv, 1, Nk, D, in_dtype, 0).  Errors: FA_ERR_NULL for a NULL table or
+ * length array, FA_ERR_DIM for page_size not a positive multiple of 64,
+ * max_pages or num_pages < 1 or page_size * max_pages above 2^31 - 1,
+ * FA_ERR_ALIGN for a table or length array not 4-byte aligned, FA_ERR_DTYPE
+ * for fp32 data, FA_ERR_HEAD_DIM for another D, FA_ERR_ALIAS when o or lse
+ * overlaps the pools, the table or the lengths; otherwise as fa_fwd. */
+fa_status_t fa_fwd_kvcache_paged(const void *q, const void *k_pages, const void *v_pages, void *o,
+                                 float *lse, const int *seqlens_k, const int *block_table, int B,
+                                 int Hq, int Hkv, int Nq, int D, int page_size, int max_pages,
+                                 int num_pages, int causal, float scale, void *stream,
+                                 fa_dtype_t in_dtype, fa_dtype_t out_dtype);
+
 /* Bytes of decode workspace a call with these sizes needs (0 when the call
  * takes no split-KV path).  num_splits as in fa_fwd_splitkv. */
 size_t fa_workspace_bytes(int B, int Hq, int Hkv, int Nq, int Nk, int D, fa_dtype_t in_dtype,

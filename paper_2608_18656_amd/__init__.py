@@ -8,7 +8,7 @@ from __future__ import annotations
 
 import math
 
-__all__ = ["fwd", "fwd_splitkv", "fwd_kvcache", "q8_0_gemv", "FaError", "validate", "workspace_bytes", "release_workspace",
+__all__ = ["fwd", "fwd_splitkv", "fwd_kvcache", "fwd_kvcache_paged", "q8_0_gemv", "FaError", "validate", "workspace_bytes", "release_workspace",
            "set_workspace", "version", "DTYPE_CODES"]
 
 
@@ -134,6 +134,63 @@ def fwd_kvcache(q, k_cache, v_cache, seqlens_k, causal: bool = False, scale: flo
                                 lse.data_ptr() if lse is not None else None, seqlens_k.data_ptr(),
                                 B, Hq, Hkv, Nq, Nk, D, int(bool(causal)), float(scale), stream,
                                 codes[q.dtype], codes.get(odt, -1))
+    _check(lib, st)
+    return out, lse
+
+
+def fwd_kvcache_paged(q, k_pages, v_pages, block_table, seqlens_k, causal: bool = False,
+                      scale: float | None = None, out=None, lse=None, out_dtype=None,
+                      return_lse: bool = True):
+    """Attention against a paged K/V cache: ``k_pages``, ``v_pages``
+    [num_pages, page_size, Hkv, D] (page_size a multiple of 64), ``block_table``
+    int32 [B, max_pages] (page of each block of page_size keys of each
+    sequence), ``seqlens_k`` int32 [B]; q [B, Nq, Hq, D] holds each sequence's
+    last Nq positions.  See fa_fwd_kvcache_paged in include/fa.h."""
+    from . import _lib
+
+    lib = _lib.load()
+    torch = _torch()
+    for name, t in (("q", q), ("k_pages", k_pages), ("v_pages", v_pages)):
+        if not t.is_cuda or not t.is_contiguous() or t.dim() != 4:
+            raise ValueError(f"{name} must be a contiguous 4-D GPU tensor")
+    if not (q.device == k_pages.device == v_pages.device):
+        raise ValueError("q and the page pools must be on the same device")
+    if not (q.dtype == k_pages.dtype == v_pages.dtype) or q.dtype not in _codes():
+        raise ValueError("q and the page pools must share one dtype")
+    if tuple(k_pages.shape) != tuple(v_pages.shape):
+        raise ValueError("k_pages and v_pages must have the same shape")
+    B, Nq, Hq, D = q.shape
+    num_pages, page_size, Hkv, Dk = k_pages.shape
+    if Dk != D:
+        raise ValueError("the page pools' head size differs from q's")
+    for name, t, shp in (("block_table", block_table, None), ("seqlens_k", seqlens_k, (B,))):
+        if (not t.is_cuda or t.dtype != torch.int32 or not t.is_contiguous() or t.device != q.device
+                or (shp is not None and tuple(t.shape) != shp)):
+            raise ValueError(f"{name} must be a contiguous int32 tensor on q's device")
+    if block_table.dim() != 2 or block_table.shape[0] != B:
+        raise ValueError("block_table must be [B, max_pages]")
+    max_pages = block_table.shape[1]
+    odt = q.dtype if out_dtype is None else out_dtype
+    if out is None:
+        out = torch.empty((B, Nq, Hq, D), dtype=odt, device=q.device)
+    elif (tuple(out.shape) != (B, Nq, Hq, D) or out.dtype != odt or not out.is_contiguous()
+          or out.device != q.device):
+        raise ValueError("out must be a contiguous [B, Nq, Hq, D] tensor of the output dtype")
+    if lse is None and return_lse:
+        lse = torch.empty((B, Hq, Nq), dtype=torch.float32, device=q.device)
+    elif lse is not None and (tuple(lse.shape) != (B, Hq, Nq) or lse.dtype != torch.float32
+                              or not lse.is_contiguous() or lse.device != q.device):
+        raise ValueError("lse must be a contiguous float32 [B, Hq, Nq] tensor")
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    codes = _codes()
+    stream = torch.cuda.current_stream(q.device).cuda_stream
+    with torch.cuda.device(q.device):
+        st = lib.fa_fwd_kvcache_paged(
+            q.data_ptr(), k_pages.data_ptr(), v_pages.data_ptr(), out.data_ptr(),
+            lse.data_ptr() if lse is not None else None, seqlens_k.data_ptr(), block_table.data_ptr(),
+            B, Hq, Hkv, Nq, D, page_size, max_pages, num_pages, int(bool(causal)), float(scale),
+            stream, codes[q.dtype], codes.get(odt, -1))
     _check(lib, st)
     return out, lse
 

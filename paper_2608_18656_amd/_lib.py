@@ -26,7 +26,7 @@ STATUS_NAMES = {
 EXPORTS = ("fa_status_string", "fa_version", "fa_validate", "fa_fwd_f16", "fa_fwd_bf16",
            "fa_fwd_f32", "fa_fwd", "fa_fwd_splitkv", "fa_workspace_bytes",
            "fa_release_workspace", "fa_set_workspace", "fa_fwd_packed", "fa_fwd_kvcache",
-           "fa_q8_0_gemv")
+           "fa_q8_0_gemv", "fa_fwd_kvcache_paged")
 
 _lib = None
 
@@ -72,5 +72,7 @@ def load():
     lib.fa_set_workspace.restype = _I
     lib.fa_q8_0_gemv.argtypes = [_P, _P, _P, _I, _I, _I, _I, _P]
     lib.fa_q8_0_gemv.restype = _I
+    lib.fa_fwd_kvcache_paged.argtypes = [_P] * 7 + [_I] * 9 + [ctypes.c_float, _P, _I, _I]
+    lib.fa_fwd_kvcache_paged.restype = _I
     _lib = lib
     return lib

@@ -67,17 +67,58 @@ fa_status_t get_workspace(size_t need, void **out, bool *user) {
     return FA_OK;
 }
 
+// The argument checks of every attention entry point.  kv_rows: rows of
+// Hkv * D elements that k and v each hold (-1: B * Nk, the contiguous layout).
+fa_status_t validate_core(const void *q, const void *k, const void *v, const void *o,
+                          const float *lse, int B, int Hq, int Hkv, int Nq, int Nk, int D,
+                          int causal, float scale, fa_dtype_t in, fa_dtype_t out, long long kv_rows) {
+    if (!q || !k || !v || !o) return FA_ERR_NULL;
+    if (B < 1 || Hq < 1 || Hkv < 1 || Nq < 1 || Nk < 1 || D < 1) return FA_ERR_DIM;
+    if (in != FA_F16 && in != FA_BF16 && in != FA_F32) return FA_ERR_DTYPE;
+    if (out != in && out != FA_F32) return FA_ERR_DTYPE;
+    if (Hq % Hkv != 0) return FA_ERR_GQA_RATIO;
+    if (D % 8 != 0 || D > 256) return FA_ERR_HEAD_DIM;
+    if (causal && Nq > Nk) return FA_ERR_CAUSAL_SHAPE;
+    if (!std::isfinite(scale)) return FA_ERR_SCALE;
+    long long nq, nk, t;
+    if (kv_rows < 0) kv_rows = (long long)B * Nk;
+    if (!mul_ok((long long)B * Nq, (long long)Hq * D, &nq) ||
+        !mul_ok(kv_rows, (long long)Hkv * D, &nk) ||
+        !mul_ok((long long)B * Hq, (long long)Nq, &t))
+        return FA_ERR_DIM;
+    const uintptr_t a16 = 15;
+    if ((reinterpret_cast<uintptr_t>(q) & a16) || (reinterpret_cast<uintptr_t>(k) & a16) ||
+        (reinterpret_cast<uintptr_t>(v) & a16) || (reinterpret_cast<uintptr_t>(o) & a16) ||
+        (reinterpret_cast<uintptr_t>(lse) & 3))
+        return FA_ERR_ALIGN;
+    const size_t qb = (size_t)nq * esize(in), kb = (size_t)nk * esize(in);
+    const size_t ob = (size_t)nq * esize(out), lb = (size_t)t * sizeof(float);
+    if (overlaps(o, ob, q, qb) || overlaps(o, ob, k, kb) || overlaps(o, ob, v, kb))
+        return FA_ERR_ALIAS;
+    if (lse && (overlaps(lse, lb, q, qb) || overlaps(lse, lb, k, kb) ||
+                overlaps(lse, lb, v, kb) || overlaps(lse, lb, o, ob)))
+        return FA_ERR_ALIAS;
+    return FA_OK;
+}
+
+struct Paging {
+    const int *block_table = nullptr;
+    int page_size = 0, max_pages = 0, num_pages = 0;
+};
+
 fa_status_t run(const void *q, const void *k, const void *v, void *o, float *lse, int B, int Hq,
                 int Hkv, int Nq, int Nk, int D, int causal, float scale, void *stream,
                 fa_dtype_t in, fa_dtype_t out, int splits_req, int hw_req = 0,
-                const int *seqlens = nullptr) {
-    fa_status_t st = fa_validate(q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, in, out);
+                const int *seqlens = nullptr, const Paging &pg = Paging()) {
+    const long long kv_rows = pg.block_table ? (long long)pg.num_pages * pg.page_size : -1;
+    fa_status_t st = validate_core(q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, in, out, kv_rows);
     if (st != FA_OK) return st;
     if (splits_req < 0 || splits_req > FA_MAX_SPLITS) return FA_ERR_SPLITS;
     if (!(hw_req == 0 || hw_req == 1 || hw_req == 2 || hw_req == 4) ||
         (hw_req > 0 && (Hq / Hkv) % hw_req != 0))
         return FA_ERR_PACKING;
-    fa::Problem p{q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, in, out, hw_req, seqlens};
+    fa::Problem p{q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, in, out, hw_req, seqlens,
+                  pg.block_table, pg.page_size, pg.max_pages, pg.num_pages};
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     hipError_t e;
     if (fa::decode_supported(Nq, D, in)) {
@@ -88,7 +129,8 @@ fa_status_t run(const void *q, const void *k, const void *v, void *o, float *lse
         st = get_workspace(need, &ws, &user);
         if (st != FA_OK) return st;
         if (user) {   // a caller-owned workspace must not overlap the call's tensors
-            const size_t qb = (size_t)B * Nq * Hq * D * esize(in), kb = (size_t)B * Nk * Hkv * D * esize(in);
+            const size_t qb = (size_t)B * Nq * Hq * D * esize(in);
+            const size_t kb = (size_t)(kv_rows < 0 ? (long long)B * Nk : kv_rows) * Hkv * D * esize(in);
             const size_t ob = (size_t)B * Nq * Hq * D * esize(out), lb = (size_t)B * Hq * Nq * sizeof(float);
             if (overlaps(ws, need, q, qb) || overlaps(ws, need, k, kb) || overlaps(ws, need, v, kb) ||
                 overlaps(ws, need, o, ob) || (lse && overlaps(ws, need, lse, lb)))
@@ -134,32 +176,7 @@ int fa_version(void) { return (0 << 16) | (1 << 8) | 0; }
 fa_status_t fa_validate(const void *q, const void *k, const void *v, const void *o,
                         const float *lse, int B, int Hq, int Hkv, int Nq, int Nk, int D,
                         int causal, float scale, fa_dtype_t in, fa_dtype_t out) {
-    if (!q || !k || !v || !o) return FA_ERR_NULL;
-    if (B < 1 || Hq < 1 || Hkv < 1 || Nq < 1 || Nk < 1 || D < 1) return FA_ERR_DIM;
-    if (in != FA_F16 && in != FA_BF16 && in != FA_F32) return FA_ERR_DTYPE;
-    if (out != in && out != FA_F32) return FA_ERR_DTYPE;
-    if (Hq % Hkv != 0) return FA_ERR_GQA_RATIO;
-    if (D % 8 != 0 || D > 256) return FA_ERR_HEAD_DIM;
-    if (causal && Nq > Nk) return FA_ERR_CAUSAL_SHAPE;
-    if (!std::isfinite(scale)) return FA_ERR_SCALE;
-    long long nq, nk, t;
-    if (!mul_ok((long long)B * Nq, (long long)Hq * D, &nq) ||
-        !mul_ok((long long)B * Nk, (long long)Hkv * D, &nk) ||
-        !mul_ok((long long)B * Hq, (long long)Nq, &t))
-        return FA_ERR_DIM;
-    const uintptr_t a16 = 15;
-    if ((reinterpret_cast<uintptr_t>(q) & a16) || (reinterpret_cast<uintptr_t>(k) & a16) ||
-        (reinterpret_cast<uintptr_t>(v) & a16) || (reinterpret_cast<uintptr_t>(o) & a16) ||
-        (reinterpret_cast<uintptr_t>(lse) & 3))
-        return FA_ERR_ALIGN;
-    const size_t qb = (size_t)nq * esize(in), kb = (size_t)nk * esize(in);
-    const size_t ob = (size_t)nq * esize(out), lb = (size_t)t * sizeof(float);
-    if (overlaps(o, ob, q, qb) || overlaps(o, ob, k, kb) || overlaps(o, ob, v, kb))
-        return FA_ERR_ALIAS;
-    if (lse && (overlaps(lse, lb, q, qb) || overlaps(lse, lb, k, kb) ||
-                overlaps(lse, lb, v, kb) || overlaps(lse, lb, o, ob)))
-        return FA_ERR_ALIAS;
-    return FA_OK;
+    return validate_core(q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, in, out, -1);
 }
 
 fa_status_t fa_fwd(const void *q, const void *k, const void *v, void *o, float *lse, int B,
@@ -218,6 +235,46 @@ fa_status_t fa_fwd_kvcache(const void *q, const void *k, const void *v, void *o,
     }
     return run(q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, stream, in_dtype, out_dtype, 0,
                0, seqlens_k);
+}
+
+fa_status_t fa_fwd_kvcache_paged(const void *q, const void *k_pages, const void *v_pages, void *o,
+                                 float *lse, const int *seqlens_k, const int *block_table, int B,
+                                 int Hq, int Hkv, int Nq, int D, int page_size, int max_pages,
+                                 int num_pages, int causal, float scale, void *stream,
+                                 fa_dtype_t in_dtype, fa_dtype_t out_dtype) {
+    if (!seqlens_k || !block_table) return FA_ERR_NULL;
+    if (page_size < 64 || page_size % 64 != 0 || max_pages < 1 || num_pages < 1 ||
+        (long long)page_size * max_pages > 0x7fffffffLL || (long long)B * max_pages > 0x7fffffffLL)
+        return FA_ERR_DIM;
+    if ((reinterpret_cast<uintptr_t>(seqlens_k) & 3) || (reinterpret_cast<uintptr_t>(block_table) & 3))
+        return FA_ERR_ALIGN;
+    const int Nk = page_size * max_pages;
+    // only the matrix-core kernels read pages
+    if (in_dtype != FA_F16 && in_dtype != FA_BF16) {
+        const fa_status_t st = validate_core(q, k_pages, v_pages, o, lse, B, Hq, Hkv, Nq, Nk, D, causal,
+                                             scale, in_dtype, out_dtype, (long long)num_pages * page_size);
+        return st != FA_OK ? st : FA_ERR_DTYPE;
+    }
+    if (D != 64 && D != 128) {
+        const fa_status_t st = validate_core(q, k_pages, v_pages, o, lse, B, Hq, Hkv, Nq, Nk, D, causal,
+                                             scale, in_dtype, out_dtype, (long long)num_pages * page_size);
+        return st != FA_OK ? st : FA_ERR_HEAD_DIM;
+    }
+    if (B >= 1 && o && Hq >= 1 && Nq >= 1) {
+        const size_t ob = (size_t)B * Nq * Hq * D * esize(out_dtype);
+        const size_t lb = (size_t)B * Hq * Nq * sizeof(float);
+        const size_t sb = (size_t)B * sizeof(int), tb = (size_t)B * max_pages * sizeof(int);
+        if (overlaps(o, ob, seqlens_k, sb) || overlaps(o, ob, block_table, tb) ||
+            (lse && (overlaps(lse, lb, seqlens_k, sb) || overlaps(lse, lb, block_table, tb))))
+            return FA_ERR_ALIAS;
+    }
+    Paging pg;
+    pg.block_table = block_table;
+    pg.page_size = page_size;
+    pg.max_pages = max_pages;
+    pg.num_pages = num_pages;
+    return run(q, k_pages, v_pages, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, stream, in_dtype,
+               out_dtype, 0, 0, seqlens_k, pg);
 }
 
 size_t fa_workspace_bytes(int B, int Hq, int Hkv, int Nq, int Nk, int D, fa_dtype_t in_dtype,

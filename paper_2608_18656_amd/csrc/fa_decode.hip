@@ -43,6 +43,8 @@ struct DecodeArgs {
     float c;        // |scale| * log2(e)
     unsigned qsign; // sign flip of q for negative scale
     const int *seqlens;   // valid keys per batch element (NULL: Nk for all)
+    const int *block_table;   // paged K/V: page of each key block (see Problem)
+    int page_size, max_pages, num_pages;
 };
 
 template <int D> struct DSmem {
@@ -60,7 +62,7 @@ __device__ __forceinline__ void wave_lds_fence() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-template <typename TIN, int D>
+template <typename TIN, int D, bool PAGED>
 __global__ __launch_bounds__(64 * NW, 1) void decode_split_kernel(DecodeArgs a) {
     using S = typename TIN::scalar;
     using V8 = typename TIN::vec8;
@@ -126,15 +128,27 @@ __global__ __launch_bounds__(64 * NW, 1) void decode_split_kernel(DecodeArgs a) 
     // the MFMA operand layout), V as fp16 (read back transposed).
     uint4_t kr[RLOADS], vr[RLOADS];   // the next chunk's rows, in flight
     auto gload = [&](int kb) {
+        // element offset of key kb's row (head g): contiguous, or through the
+        // block table (a chunk never crosses a page: chunks start at multiples
+        // of 32 keys and pages hold a multiple of 64; page numbers are clamped
+        // into the pool)
+        size_t rbase;
+        if constexpr (PAGED) {
+            const int pi = kb / a.page_size;
+            const int page = min(max(a.block_table[(size_t)b * a.max_pages + pi], 0), a.num_pages - 1);
+            rbase = ((size_t)page * a.page_size + (kb - pi * a.page_size)) * row_stride + (size_t)g * D;
+        } else {
+            rbase = head_off + (size_t)kb * row_stride;
+        }
 #pragma unroll
         for (int i = 0; i < RLOADS; ++i) {
             const int c = l + 64 * i;
-            const int key = kb + c / CPR, cc = c % CPR;
+            const int kc = c / CPR, cc = c % CPR;
             kr[i] = uint4_t{0u, 0u, 0u, 0u};
             vr[i] = uint4_t{0u, 0u, 0u, 0u};
-            if (key < k1) {
-                kr[i] = ld16_stream(kbase + head_off + key * row_stride + 8 * cc);
-                vr[i] = ld16_stream(vbase + head_off + key * row_stride + 8 * cc);
+            if (kb + kc < k1) {
+                kr[i] = ld16_stream(kbase + rbase + kc * row_stride + 8 * cc);
+                vr[i] = ld16_stream(vbase + rbase + kc * row_stride + 8 * cc);
             }
         }
     };
@@ -332,10 +346,18 @@ hipError_t launch_t(const Problem &p, int S, void *ws, hipStream_t stream) {
     a.c = __builtin_fabsf(p.scale) * kLog2e;
     a.qsign = p.scale < 0.f ? 0x80008000u : 0u;
     a.seqlens = p.seqlens;
+    a.block_table = p.block_table;
+    a.page_size = p.page_size;
+    a.max_pages = p.max_pages;
+    a.num_pages = p.num_pages;
     const long long nblocks = (long long)p.B * p.Hkv * a.nqg * S;
     if (nblocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL((decode_split_kernel<TIN, D>), dim3((unsigned)nblocks), dim3(64 * NW), 0,
-                       stream, a);
+    if (p.block_table)
+        hipLaunchKernelGGL((decode_split_kernel<TIN, D, true>), dim3((unsigned)nblocks), dim3(64 * NW), 0,
+                           stream, a);
+    else
+        hipLaunchKernelGGL((decode_split_kernel<TIN, D, false>), dim3((unsigned)nblocks), dim3(64 * NW), 0,
+                           stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((decode_combine_kernel<TOUT, D>), dim3((unsigned)(p.B * p.Hq)), dim3(D), 0,

@@ -19,6 +19,11 @@ struct Problem {
     fa_dtype_t in, out;
     int hw;   // prefill query heads per workgroup (0: the default choice)
     const int *seqlens;   // device [B]: valid keys per batch element (NULL: Nk for all)
+    // Paged K/V (block_table != NULL): k and v are [num_pages][page_size][Hkv][D];
+    // key j of batch element b is row j % page_size of page
+    // block_table[b * max_pages + j / page_size]; Nk = page_size * max_pages.
+    const int *block_table;
+    int page_size, max_pages, num_pages;
 };
 
 // Each launcher enqueues its kernels on `stream` and returns the first HIP

@@ -63,6 +63,8 @@ struct PrefillArgs {
     int nhg;          // head groups per key/value head (G / HW)
     int pair;         // 1: every workgroup is resident at once; order heavy/light pairs
     const int *seqlens;   // valid keys per batch element (NULL: Nk for all)
+    const int *block_table;   // paged K/V: page of each key block (see Problem)
+    int page_size, max_pages, num_pages;
 };
 
 // Tile shape per head size.  Every wave handles 32 query rows and 32 keys of
@@ -88,7 +90,7 @@ template <int D> struct Cfg {
     static constexpr int WORDS = (NSTAGE * STAGE) > (2 * MERGE) ? NSTAGE * STAGE : 2 * MERGE;
 };
 
-template <typename TIN, typename TOUT, int D, bool CAUSAL>
+template <typename TIN, typename TOUT, int D, bool CAUSAL, bool PAGED>
 __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<D>::WPE, Cfg<D>::WPE))) void prefill_kernel(PrefillArgs a) {
     using S = typename TIN::scalar;
     using V8 = typename TIN::vec8;
@@ -191,7 +193,19 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
     const S *tnext = kvbase;
     long long rem = (long long)(Nk - 1) * (long long)row_elems * (long long)sizeof(S) +
                     (long long)D * (long long)sizeof(S);
-    auto gload = [&](int) {   // the next tile (tiles are loaded in order; the argument is its first key)
+    // paged K/V: the pool of pages, at head g
+    const S *kvpool = reinterpret_cast<const S *>(kgroup ? a.k : a.v) + (size_t)g * D;
+    auto gload = [&](int kt) {   // the next tile (tiles are loaded in order; the argument is its first key)
+        if constexpr (PAGED) {
+            // the tile's rows sit in one page (pages hold a multiple of 64
+            // keys, tiles start at multiples of BC); the view ends after the
+            // last valid key of the tile; page numbers are clamped into the pool
+            const int pi = kt / a.page_size;
+            const int page = min(max(a.block_table[(size_t)b * a.max_pages + pi], 0), a.num_pages - 1);
+            tnext = kvpool + ((size_t)page * a.page_size + (kt - pi * a.page_size)) * row_elems;
+            rem = (long long)(min(Nk - kt, BC) - 1) * (long long)row_elems * (long long)sizeof(S) +
+                  (long long)D * (long long)sizeof(S);
+        }
         // view range, clamped to 31 bits (the tile's own extent always fits);
         // the halves are opaque so that the test stays two 32-bit scalar
         // compares instead of one 64-bit vector compare
@@ -203,8 +217,10 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
 #pragma unroll
         for (int i = 0; i < SL; ++i)
             sr[i] = __builtin_bit_cast(uint4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, goff[i], 0, 0));
-        tnext += (size_t)BC * row_elems;
-        rem -= (long long)BC * (long long)row_elems * (long long)sizeof(S);
+        if constexpr (!PAGED) {
+            tnext += (size_t)BC * row_elems;
+            rem -= (long long)BC * (long long)row_elems * (long long)sizeof(S);
+        }
     };
     // LDS destination (element offset inside a stage) of load i
     auto sdst = [&](int i) {
@@ -522,6 +538,10 @@ hipError_t launch_t(const Problem &p, hipStream_t stream) {
     a.q = p.q; a.k = p.k; a.v = p.v; a.o = p.o; a.lse = p.lse;
     a.B = p.B; a.Hq = p.Hq; a.Hkv = p.Hkv; a.Nq = p.Nq; a.Nk = p.Nk;
     a.seqlens = p.seqlens;
+    a.block_table = p.block_table;
+    a.page_size = p.page_size;
+    a.max_pages = p.max_pages;
+    a.num_pages = p.num_pages;
     // A zero scale keeps a tiny positive factor: every visible exponent is then
     // exactly 0 in fp32, and masked (-inf) scores still give 0.
     a.c = __builtin_fmaxf(__builtin_fabsf(p.scale), 1e-30f) * kLog2e;
@@ -536,8 +556,12 @@ hipError_t launch_t(const Problem &p, hipStream_t stream) {
     if (nblocks <= 0) return hipSuccess;
     if (nblocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     if (p.causal) a.pair = nblocks <= (long long)Cfg<D>::WPC * cu_count() ? 1 : 0;
-    hipLaunchKernelGGL((prefill_kernel<TIN, TOUT, D, CAUSAL>), dim3((unsigned)nblocks), dim3(Cfg<D>::NT),
-                       0, stream, a);
+    if (p.block_table)
+        hipLaunchKernelGGL((prefill_kernel<TIN, TOUT, D, CAUSAL, true>), dim3((unsigned)nblocks),
+                           dim3(Cfg<D>::NT), 0, stream, a);
+    else
+        hipLaunchKernelGGL((prefill_kernel<TIN, TOUT, D, CAUSAL, false>), dim3((unsigned)nblocks),
+                           dim3(Cfg<D>::NT), 0, stream, a);
     return hipGetLastError();
 }
 

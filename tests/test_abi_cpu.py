@@ -140,3 +140,27 @@ def test_q8_gemv_argument_errors_before_any_launch():
     assert call(y=W + 100) == 8                    # y inside w (8 * 2 * 34 bytes)
     assert call(y=X + 64) == 8                     # y inside x
     assert call(y=W + 8 * 2 * 34) != 8             # y right after w: no overlap reported
+
+
+def test_paged_argument_errors_before_any_launch():
+    """fa_fwd_kvcache_paged's own checks (fake addresses, no HIP call)."""
+    lib = _lib.load()
+    Q, K, V, O, L, S, T = (k << 24 for k in (1, 2, 3, 4, 5, 6, 7))
+    F16, BF16, F32 = _lib.FA_F16, _lib.FA_BF16, _lib.FA_F32
+
+    def call(q=Q, k=K, v=V, o=O, lse=L, sl=S, bt=T, B=2, Hq=8, Hkv=2, Nq=1, D=64, ps=64, mp=4, npg=8,
+             causal=0, scale=0.125, it=F16, ot=F16):
+        return lib.fa_fwd_kvcache_paged(q, k, v, o, lse, sl, bt, B, Hq, Hkv, Nq, D, ps, mp, npg, causal,
+                                        scale, None, it, ot)
+
+    assert call(sl=None) == 1 and call(bt=None) == 1 and call(q=None) == 1
+    for ps in (0, 32, 96, -64):
+        assert call(ps=ps) == 2, ps
+    assert call(mp=0) == 2 and call(npg=0) == 2 and call(ps=1 << 30, mp=4) == 2
+    assert call(sl=S + 2) == 7 and call(bt=T + 1) == 7
+    assert call(it=F32, ot=F32) == 9
+    assert call(D=96) == 4 and call(D=256) == 4
+    assert call(o=T) == 8                          # o overlaps the block table
+    assert call(lse=S) == 8                        # lse overlaps the lengths
+    assert call(o=K + 64) == 8                     # o inside the K pool (8 pages of 64 x 2 x 64 x 2 B)
+    assert call(Hq=6, Hkv=4) == 3
