@@ -21,8 +21,10 @@
 //
 // x is staged once per workgroup in LDS as fp32 (16-byte loads, all in flight
 // together; four floats of padding after every 64, so that lanes reading x
-// at a stride of 64 elements hit different banks); for K too large for LDS a
-// lane loads the slice of x its unit needs.  Products are accumulated in
+// at a stride of 64 elements hit different banks); rows of more than 15168
+// weights use 16-wave workgroups whose x takes up to the 160 KB of LDS a
+// workgroup may hold, and for longer rows a lane loads the slice of x its
+// unit needs.  Products are accumulated in
 // fp32: each int8 value is widened exactly (one sign-extending convert),
 // multiplied by x and summed per block, then scaled and added to the lane's
 // sum; the L lanes of a row are summed with DPP row shifts and broadcasts.
@@ -43,9 +45,11 @@ namespace fa {
 namespace {
 
 constexpr int Q8_NT = 256;              // threads per workgroup (4 waves)
-constexpr int Q8_WAVES = Q8_NT / 64;
-constexpr int Q8_XLDS_MAX = 15168;      // largest K staged in LDS ((K + K/16) floats and the
-                                        // result buffers within 64 KB)
+constexpr int Q8_NT_WIDE = 1024;        // threads per workgroup for long rows (16 waves)
+constexpr int Q8_XLDS_MAX = 15168;      // largest K staged in LDS by a 4-wave workgroup ((K + K/16)
+                                        // floats and the result buffers within 64 KB)
+constexpr int Q8_XLDS_WIDE_MAX = 37568; // largest K staged by a 16-wave workgroup (within the
+                                        // 160 KB of LDS a workgroup may hold on gfx950)
 constexpr int Q8_DEPTH = 2;             // units in flight per lane
 constexpr int Q8_MAX_WG = 256 * 4;      // grid cap: workgroups (rows are strided beyond it)
 
@@ -193,13 +197,14 @@ __device__ __forceinline__ float segment_sum(float v, int L) {
 // the loads of the unit DEPTH - 1 rounds ahead are issued before the current
 // unit is computed.  Results of finished rows go to a per-wave LDS buffer and
 // are written to y in bursts, so that stores seldom stand between loads.
-template <typename TX, typename TY, bool PAIR, int XM, int DEPTH>
-__global__ __launch_bounds__(Q8_NT) void q8_gemv_kernel(const unsigned char *__restrict__ w,
+template <typename TX, typename TY, bool PAIR, int XM, int DEPTH, int NT>
+__global__ __launch_bounds__(NT) void q8_gemv_kernel(const unsigned char *__restrict__ w,
                                                         const TX *__restrict__ x, TY *__restrict__ y,
                                                         int M, int K, int L) {
     extern __shared__ __align__(16) float smem[];
     constexpr int UW = PAIR ? 64 : 32;                     // weights per unit
     constexpr unsigned UB = PAIR ? 68 : 34;                // bytes per unit
+    constexpr int WAVES = NT / 64;
     const int nb = K / 32;
     const int units = PAIR ? nb / 2 : nb;                  // units per row
     const int rounds = (units + L - 1) / L;                // rounds of lanes per row group
@@ -207,8 +212,8 @@ __global__ __launch_bounds__(Q8_NT) void q8_gemv_kernel(const unsigned char *__r
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: the view lives in SGPRs
     const int R = 64 / L;
     const int sub = lane / L, sl = lane % L;
-    const long long NW = (long long)gridDim.x * Q8_WAVES;
-    const long long wv = (long long)blockIdx.x * Q8_WAVES + wave;
+    const long long NW = (long long)gridDim.x * WAVES;
+    const long long wv = (long long)blockIdx.x * WAVES + wave;
     const long long groups = ((long long)M + R - 1) / R;
     const long long my_groups = wv < groups ? (groups - wv + NW - 1) / NW : 0;
     const long long steps = my_groups * rounds;
@@ -246,16 +251,16 @@ __global__ __launch_bounds__(Q8_NT) void q8_gemv_kernel(const unsigned char *__r
     if constexpr (XM == X_LDS) {
         constexpr int E = 16 / sizeof(TX);
         const int C = K / E;                                // 16-byte chunks of x
-        for (int c0 = tid; c0 < C; c0 += 4 * Q8_NT) {
+        for (int c0 = tid; c0 < C; c0 += 4 * NT) {
             u32x4 v[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int c = c0 + i * Q8_NT;
+                const int c = c0 + i * NT;
                 if (c < C) v[i] = reinterpret_cast<const u32x4 *>(x)[c];
             }
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int c = c0 + i * Q8_NT;
+                const int c = c0 + i * NT;
                 if (c < C) {
                     float f[E];
                     widen16<TX>(v[i], f);
@@ -336,19 +341,29 @@ hipError_t launch_q8_t(const void *w, const void *x, void *y, int M, int K, hipS
     while (L > 16 && L / 2 >= units) L /= 2;        // rows short of work share a wave
     const int R = 64 / L;
     const long long waves_needed = ((long long)M + R - 1) / R;
-    long long blocks = (waves_needed + Q8_WAVES - 1) / Q8_WAVES;
-    if (blocks > Q8_MAX_WG) blocks = Q8_MAX_WG;
     const auto *wp = reinterpret_cast<const unsigned char *>(w);
     const auto *xp = reinterpret_cast<const TX *>(x);
     auto *yp = reinterpret_cast<TY *>(y);
-    const size_t ylds = (size_t)Q8_WAVES * Q8_YB * sizeof(float);
-    const dim3 grid((unsigned)blocks), block(Q8_NT);
-    if (K <= Q8_XLDS_MAX) {
-        hipLaunchKernelGGL((q8_gemv_kernel<TX, TY, PAIR, X_LDS, Q8_DEPTH>), grid, block,
-                           (size_t)(K + K / 16) * sizeof(float) + ylds, s, wp, xp, yp, M, K, L);
+    const size_t xlds = (size_t)(K + K / 16) * sizeof(float);
+    if (K <= Q8_XLDS_MAX || K > Q8_XLDS_WIDE_MAX) {
+        long long blocks = (waves_needed + Q8_NT / 64 - 1) / (Q8_NT / 64);
+        if (blocks > Q8_MAX_WG) blocks = Q8_MAX_WG;
+        const dim3 grid((unsigned)blocks), block(Q8_NT);
+        const size_t ylds = (size_t)(Q8_NT / 64) * Q8_YB * sizeof(float);
+        if (K <= Q8_XLDS_MAX)
+            hipLaunchKernelGGL((q8_gemv_kernel<TX, TY, PAIR, X_LDS, Q8_DEPTH, Q8_NT>), grid, block, xlds + ylds, s,
+                               wp, xp, yp, M, K, L);
+        else
+            hipLaunchKernelGGL((q8_gemv_kernel<TX, TY, PAIR, X_GLOBAL, Q8_DEPTH, Q8_NT>), grid, block, ylds, s,
+                               wp, xp, yp, M, K, L);
     } else {
-        hipLaunchKernelGGL((q8_gemv_kernel<TX, TY, PAIR, X_GLOBAL, Q8_DEPTH>), grid, block, ylds, s, wp, xp, yp,
-                           M, K, L);
+        // long rows: x of more than 64 KB, staged once by a 16-wave workgroup
+        // (one or two per CU, as the LDS allows)
+        long long blocks = (waves_needed + Q8_NT_WIDE / 64 - 1) / (Q8_NT_WIDE / 64);
+        if (blocks > Q8_MAX_WG / 2) blocks = Q8_MAX_WG / 2;
+        const size_t ylds = (size_t)(Q8_NT_WIDE / 64) * Q8_YB * sizeof(float);
+        hipLaunchKernelGGL((q8_gemv_kernel<TX, TY, PAIR, X_LDS, Q8_DEPTH, Q8_NT_WIDE>), dim3((unsigned)blocks),
+                           dim3(Q8_NT_WIDE), xlds + ylds, s, wp, xp, yp, M, K, L);
     }
     return hipGetLastError();
 }

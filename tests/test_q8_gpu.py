@@ -16,7 +16,7 @@ for bf16).
 
 Coverage: every input/output dtype pair; K of one block, odd block counts
 (the 16-bit load path), even counts with a ragged last round of lanes, the
-largest K whose x is staged in LDS and the first K beyond it; grid-stride
+largest K each workgroup size stages in LDS and the first K beyond it; grid-stride
 row counts; the four TinyLlama-shaped projection matrices at full size;
 extreme scales (largest binary16, subnormal, zero, negative) and int8 -128;
 determinism; a non-default stream; a weight matrix of more than 2^31 bytes.
@@ -85,10 +85,13 @@ SHAPES = [
     (100, 5632),         # feed-forward width (176 blocks)
     (64, 4160),          # 130 blocks: 65 pairs, a ragged second round of lanes
     (9, 32 * 131),       # odd, several rounds of lanes
-    (33, 15168),         # largest K staged in LDS
-    (17, 15200),         # first K read from global memory
+    (33, 15168),         # largest K staged in LDS by a 4-wave workgroup
+    (17, 15200),         # first K staged by a 16-wave workgroup (LDS beyond 64 KB)
     (6, 16384),
-    (5, 32 * 1001),      # odd and beyond the LDS limit
+    (5, 32 * 1001),      # odd, 16-wave workgroup
+    (3, 37568),          # largest K staged in LDS
+    (2, 37600),          # first K whose x is read from global memory
+    (2, 32 * 1201),      # odd, x from global memory
 ]
 
 
