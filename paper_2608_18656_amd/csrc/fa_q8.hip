@@ -34,7 +34,7 @@
 // its next unit before it computes the current one; no load sits behind a
 // branch, so each wait covers exactly the unit it needs.  Finished rows go to
 // a small LDS buffer and are written out in bursts.  The grid is capped at
-// four workgroups per CU and strides over row groups.
+// 1024 four-wave (or 512 sixteen-wave) workgroups and strides over row groups.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
