@@ -244,32 +244,47 @@ __global__ __launch_bounds__(NT) void q8_gemv_kernel(const unsigned char *__rest
         }
     };
 
+    // x is staged in batches of 4 x NT 16-byte chunks.  The first batch's
+    // loads are issued before the first unit's (the wait for an older load
+    // does not cover a newer one, so x can be staged while W is in flight);
+    // loads past the end of x read zero (a buffer view of x), so none sits
+    // behind a branch.
+    constexpr int E = 16 / sizeof(TX);
+    const int C = K / E;                                    // 16-byte chunks of x
+    const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<TX *>(x), (short)0, XM == X_LDS ? C * 16 : 0, 0x00020000);
+    u32x4 xv[4];
+    auto xload = [&](int c0) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            xv[i] = __builtin_bit_cast(
+                u32x4, __builtin_amdgcn_raw_buffer_load_b128(xrs, (unsigned)(c0 + tid + i * NT) * 16u, 0, 0));
+    };
+    auto xstore = [&](int c0) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int c = c0 + tid + i * NT;
+            if (c < C) {
+                float f[E];
+                widen16<TX>(xv[i], f);
+                float *dst = xs + xslot(c * E);             // E consecutive slots, 16-byte aligned
+#pragma unroll
+                for (int j = 0; j < E; j += 4)
+                    *reinterpret_cast<f32x4 *>(dst + j) = f32x4{f[j], f[j + 1], f[j + 2], f[j + 3]};
+            }
+        }
+    };
+    if constexpr (XM == X_LDS) xload(0);
+
     Unit<PAIR> b[DEPTH];
 #pragma unroll
     for (int i = 0; i < DEPTH - 1; ++i) fetch(b[i]);
 
     if constexpr (XM == X_LDS) {
-        constexpr int E = 16 / sizeof(TX);
-        const int C = K / E;                                // 16-byte chunks of x
-        for (int c0 = tid; c0 < C; c0 += 4 * NT) {
-            u32x4 v[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int c = c0 + i * NT;
-                if (c < C) v[i] = reinterpret_cast<const u32x4 *>(x)[c];
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int c = c0 + i * NT;
-                if (c < C) {
-                    float f[E];
-                    widen16<TX>(v[i], f);
-                    float *dst = xs + xslot(c * E);         // E consecutive slots, 16-byte aligned
-#pragma unroll
-                    for (int j = 0; j < E; j += 4)
-                        *reinterpret_cast<f32x4 *>(dst + j) = f32x4{f[j], f[j + 1], f[j + 2], f[j + 3]};
-                }
-            }
+        xstore(0);
+        for (int c0 = 4 * NT; c0 < C; c0 += 4 * NT) {       // long rows: the further batches
+            xload(c0);
+            xstore(c0);
         }
         __syncthreads();
     }
