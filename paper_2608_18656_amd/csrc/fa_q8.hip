@@ -197,26 +197,32 @@ __device__ __forceinline__ float segment_sum(float v, int L) {
 // the loads of the unit DEPTH - 1 rounds ahead are issued before the current
 // unit is computed.  Results of finished rows go to a per-wave LDS buffer and
 // are written to y in bursts, so that stores seldom stand between loads.
+// Launch constants, computed on the host (so that a wave starts its loads
+// without integer divisions): L lanes per row (a power of two, 2^lgL), R =
+// 64 / L = 2^lgR rows per group, units per row, rounds = ceil(units / L) and
+// the number of row groups.
+struct Q8Args {
+    int M, K, L, lgL, lgR, units, rounds, groups;
+};
+
 template <typename TX, typename TY, bool PAIR, int XM, int DEPTH, int NT>
 __global__ __launch_bounds__(NT) void q8_gemv_kernel(const unsigned char *__restrict__ w,
                                                         const TX *__restrict__ x, TY *__restrict__ y,
-                                                        int M, int K, int L) {
+                                                        Q8Args a) {
     extern __shared__ __align__(16) float smem[];
     constexpr int UW = PAIR ? 64 : 32;                     // weights per unit
     constexpr unsigned UB = PAIR ? 68 : 34;                // bytes per unit
     constexpr int WAVES = NT / 64;
+    const int M = a.M, K = a.K, L = a.L, units = a.units, rounds = a.rounds, groups = a.groups;
     const int nb = K / 32;
-    const int units = PAIR ? nb / 2 : nb;                  // units per row
-    const int rounds = (units + L - 1) / L;                // rounds of lanes per row group
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: the view lives in SGPRs
-    const int R = 64 / L;
-    const int sub = lane / L, sl = lane % L;
-    const long long NW = (long long)gridDim.x * WAVES;
-    const long long wv = (long long)blockIdx.x * WAVES + wave;
-    const long long groups = ((long long)M + R - 1) / R;
-    const long long my_groups = wv < groups ? (groups - wv + NW - 1) / NW : 0;
-    const long long steps = my_groups * rounds;
+    const int R = 1 << a.lgR;
+    const int sub = lane >> a.lgL, sl = lane & (L - 1);
+    const int NW = (int)gridDim.x * WAVES;                  // waves in the grid
+    const int wv = (int)blockIdx.x * WAVES + wave;          // this wave's index
+    const int my_groups = wv < groups ? (int)((unsigned)(groups - 1 - wv) / (unsigned)NW) + 1 : 0;
+    const int steps = my_groups * rounds;
     const unsigned row_bytes = (unsigned)nb * 34u;           // R > 1 only for rows of <= 2176 bytes
     const long long group_bytes = (long long)R * row_bytes;
     float *xs = smem;
@@ -225,7 +231,7 @@ __global__ __launch_bounds__(NT) void q8_gemv_kernel(const unsigned char *__rest
     // fetch cursor: the group's first byte and the bytes from there to the
     // end of W (the view, clamped to 31 bits), and the round within the group
     const unsigned char *fbase = w + (size_t)wv * (size_t)group_bytes;
-    long long frem = (long long)M * row_bytes - wv * group_bytes;
+    long long frem = (long long)M * row_bytes - (long long)wv * group_bytes;
     int fr = 0;
     auto fetch = [&](Unit<PAIR> &t) {
         unsigned rlo = (unsigned)frem, rhi = (unsigned)(frem >> 32);
@@ -240,7 +246,7 @@ __global__ __launch_bounds__(NT) void q8_gemv_kernel(const unsigned char *__rest
         if (++fr == rounds) {
             fr = 0;
             fbase += (size_t)NW * (size_t)group_bytes;
-            frem -= NW * group_bytes;
+            frem -= (long long)NW * group_bytes;
         }
     };
 
@@ -290,16 +296,16 @@ __global__ __launch_bounds__(NT) void q8_gemv_kernel(const unsigned char *__rest
     }
 
     // compute cursor
-    long long g_done = 0;          // groups of this wave finished
-    long long g_flushed = 0;       // of which written to y
+    int g_done = 0;                // groups of this wave finished
+    int g_flushed = 0;             // of which written to y
     int cr = 0;
     float acc = 0.f;
     auto flush = [&]() {
-        const int n = (int)(g_done - g_flushed) * R;       // entries in the buffer
+        const int n = (g_done - g_flushed) * R;            // entries in the buffer
         __builtin_amdgcn_wave_barrier();
         if (lane < n) {
-            const long long g = wv + (g_flushed + lane / R) * NW;
-            const long long m = g * R + lane % R;
+            const long long g = wv + (long long)(g_flushed + (lane >> a.lgR)) * NW;
+            const long long m = g * R + (lane & (R - 1));
             if (m < M) y[m] = (TY)ybuf[lane];
         }
         __builtin_amdgcn_wave_barrier();
@@ -322,14 +328,14 @@ __global__ __launch_bounds__(NT) void q8_gemv_kernel(const unsigned char *__rest
             cr = 0;
             // group done: each row's sum over its L lanes lands in its last lane
             acc = segment_sum(acc, L);
-            if (sl == L - 1) ybuf[(int)(g_done - g_flushed) * R + sub] = acc;
+            if (sl == L - 1) ybuf[(g_done - g_flushed) * R + sub] = acc;
             acc = 0.f;
             ++g_done;
-            if ((int)(g_done - g_flushed) * R == Q8_YB) flush();
+            if ((g_done - g_flushed) * R == Q8_YB) flush();
         }
     };
 
-    long long t = 0;
+    int t = 0;
     for (; t + DEPTH <= steps; t += DEPTH) {
 #pragma unroll
         for (int s = 0; s < DEPTH; ++s) {
@@ -350,12 +356,20 @@ __global__ __launch_bounds__(NT) void q8_gemv_kernel(const unsigned char *__rest
 
 template <typename TX, typename TY, bool PAIR>
 hipError_t launch_q8_t(const void *w, const void *x, void *y, int M, int K, hipStream_t s) {
-    const int nb = K / 32;
-    const int units = PAIR ? nb / 2 : nb;           // lane work items per row
-    int L = 64;
-    while (L > 16 && L / 2 >= units) L /= 2;        // rows short of work share a wave
-    const int R = 64 / L;
-    const long long waves_needed = ((long long)M + R - 1) / R;
+    Q8Args a;
+    a.M = M;
+    a.K = K;
+    a.units = PAIR ? K / 64 : K / 32;                   // lane work items per row
+    a.L = 64;
+    a.lgL = 6;
+    while (a.L > 16 && a.L / 2 >= a.units) {            // rows short of work share a wave
+        a.L /= 2;
+        --a.lgL;
+    }
+    a.lgR = 6 - a.lgL;
+    a.rounds = (a.units + a.L - 1) / a.L;
+    a.groups = (int)(((long long)M + (1 << a.lgR) - 1) >> a.lgR);
+    const long long waves_needed = a.groups;            // one wave per row group at most
     const auto *wp = reinterpret_cast<const unsigned char *>(w);
     const auto *xp = reinterpret_cast<const TX *>(x);
     auto *yp = reinterpret_cast<TY *>(y);
@@ -367,10 +381,10 @@ hipError_t launch_q8_t(const void *w, const void *x, void *y, int M, int K, hipS
         const size_t ylds = (size_t)(Q8_NT / 64) * Q8_YB * sizeof(float);
         if (K <= Q8_XLDS_MAX)
             hipLaunchKernelGGL((q8_gemv_kernel<TX, TY, PAIR, X_LDS, Q8_DEPTH, Q8_NT>), grid, block, xlds + ylds, s,
-                               wp, xp, yp, M, K, L);
+                               wp, xp, yp, a);
         else
             hipLaunchKernelGGL((q8_gemv_kernel<TX, TY, PAIR, X_GLOBAL, Q8_DEPTH, Q8_NT>), grid, block, ylds, s,
-                               wp, xp, yp, M, K, L);
+                               wp, xp, yp, a);
     } else {
         // long rows: x of more than 64 KB, staged once by a 16-wave workgroup
         // (one or two per CU, as the LDS allows)
@@ -378,7 +392,7 @@ hipError_t launch_q8_t(const void *w, const void *x, void *y, int M, int K, hipS
         if (blocks > Q8_MAX_WG / 2) blocks = Q8_MAX_WG / 2;
         const size_t ylds = (size_t)(Q8_NT_WIDE / 64) * Q8_YB * sizeof(float);
         hipLaunchKernelGGL((q8_gemv_kernel<TX, TY, PAIR, X_LDS, Q8_DEPTH, Q8_NT_WIDE>), dim3((unsigned)blocks),
-                           dim3(Q8_NT_WIDE), xlds + ylds, s, wp, xp, yp, M, K, L);
+                           dim3(Q8_NT_WIDE), xlds + ylds, s, wp, xp, yp, a);
     }
     return hipGetLastError();
 }
