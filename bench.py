@@ -87,6 +87,48 @@ def time_calls(torch, fns, steps, warmup):
     return t0.elapsed_time(t1) / steps
 
 
+def loaded_sclk_mhz(torch, call, seconds=2.0):
+    """Shader clock (MHz, mean over the XCDs and two samples) read with amd-smi
+    right after `call` has been queued back to back for about `seconds`
+    (replayed from a HIP graph; queueing a replay takes about as long as the
+    GPU takes to run it, so the samples fall while work is still queued);
+    None when amd-smi is missing or its output cannot be read."""
+    import shutil
+    import subprocess
+
+    if shutil.which("amd-smi") is None:
+        return None
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        for _ in range(2):
+            call()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        for _ in range(20):
+            call()
+    clocks = []
+    try:
+        t_end = time.time() + seconds
+        while time.time() < t_end:
+            g.replay()
+        for _ in range(2):
+            out = subprocess.run(["amd-smi", "metric", "--clock", "--json"], capture_output=True,
+                                 text=True, timeout=20).stdout
+            data = json.loads(out[out.index("{"):])
+            gpus = data.get("gpu_data", data) if isinstance(data, dict) else data
+            for gpu in (gpus if isinstance(gpus, list) else [gpus])[:1]:
+                for name, blk in gpu.get("clock", {}).items():
+                    if name.lower().startswith("gfx") and isinstance(blk, dict):
+                        clocks.append(float(blk["clk"]["value"]))
+    except (OSError, subprocess.SubprocessError, ValueError, KeyError, TypeError):
+        clocks = []
+    torch.cuda.synchronize()
+    del g
+    return round(sum(clocks) / len(clocks), 1) if clocks else None
+
+
 def run_workload(torch, fa, w, steps, warmup, kv_sets=1, num_splits=None, packing=None):
     from paper_2608_18656_amd.inputs import make_workload
 
@@ -319,6 +361,11 @@ def main():
         algo = w.flops()
         kname, ksrc = "prefill_kernel", PREFILL_SOURCES
     log(f"[bench] {w.name}: {ms * 1e3:.1f} us/call, {value:.1f} {unit}")
+    # shader clock under this workload's load, against the 2.4 GHz the peaks assume
+    qd, kd, vd = inputs
+    sclk = loaded_sclk_mhz(torch, lambda: fa.fwd(qd, kd, vd, causal=w.causal, scale=w.softmax_scale,
+                                                 out=out, lse=lse))
+    log(f"[bench] shader clock under load: {sclk} MHz (peaks assume 2400)")
     result = {
         "metric": METRIC, "value": round(value, 3), "unit": unit, "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 6),
@@ -331,7 +378,10 @@ def main():
                      "frac": round(value / peak, 4),
                      "traffic": stored_traffic(kname, w.name, ksrc),
                      "kernel": kname, "algorithmic_per_launch": algo,
-                     "launch_us": round(ms * 1e3, 3)},
+                     "launch_us": round(ms * 1e3, 3),
+                     "sclk_mhz_under_load": sclk,
+                     "frac_at_measured_sclk": (round(value / (peak * sclk / 2400.0), 4)
+                                               if sclk and bound == "mfma" else None)},
     }
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline: oracle on host cores")
