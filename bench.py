@@ -326,6 +326,8 @@ def main():
     ap.add_argument("--workload", default="gqa_prefill_bf16")
     ap.add_argument("--no-extras", action="store_true", help="headline workload only")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sclk", action="store_true",
+                    help="skip the shader-clock reading under load (a burst of headline calls)")
     ap.add_argument("--no-ablation", action="store_true",
                     help="skip the inter-head packing ablation (e.g. under a kernel trace)")
     args = ap.parse_args()
@@ -363,8 +365,8 @@ def main():
     log(f"[bench] {w.name}: {ms * 1e3:.1f} us/call, {value:.1f} {unit}")
     # shader clock under this workload's load, against the 2.4 GHz the peaks assume
     qd, kd, vd = inputs
-    sclk = loaded_sclk_mhz(torch, lambda: fa.fwd(qd, kd, vd, causal=w.causal, scale=w.softmax_scale,
-                                                 out=out, lse=lse))
+    sclk = None if args.no_sclk else loaded_sclk_mhz(
+        torch, lambda: fa.fwd(qd, kd, vd, causal=w.causal, scale=w.softmax_scale, out=out, lse=lse))
     log(f"[bench] shader clock under load: {sclk} MHz (peaks assume 2400)")
     result = {
         "metric": METRIC, "value": round(value, 3), "unit": unit, "n_gpus": 1,
