@@ -449,7 +449,9 @@ def main():
         for ps in (64, 256):
             pus, pgbs = paged_decode(torch, fa, xw, max(5, min(args.steps, 30)), 3, ps)
             paged["pages"].append({"page_size": ps, "us_per_call": round(pus, 2), "value": round(pgbs, 1),
-                                   "unit": "GB/s", "frac": round(pgbs / PEAK_HBM_GBS, 4)})
+                                   "unit": "GB/s", "frac": round(pgbs / PEAK_HBM_GBS, 4),
+                                   "traffic": stored_traffic("decode_split_kernel",
+                                                             f"{xw.name}_paged{ps}", DECODE_SOURCES)})
             log(f"[bench] paged decode, pages of {ps}: {pus:.1f} us/call, {pgbs:.0f} GB/s")
         result["paged_decode"] = paged
         result["q8_0_gemv"] = q8_decode_step(torch, fa, max(5, min(args.steps, 20)), 3,

@@ -7,7 +7,11 @@ HBM byte counters).
     python3 paper_2608_18656_amd/profile_run.py q8_gate_up 5
 
 ``q8_<name>`` runs the Q8_0 matrix-vector product of one TinyLlama-shaped
-projection (qkv, o, gate_up or down; bf16 activations).
+projection (qkv, o, gate_up or down; bf16 activations); ``paged_<workload>
+<page_size>`` runs a decode workload against its K/V scattered over pages
+of that size in a seeded random order.
+
+    python3 paper_2608_18656_amd/profile_run.py paged_gqa_decode_bf16 256 5
 """
 from __future__ import annotations
 
@@ -34,6 +38,25 @@ def main(argv):
     import paper_2608_18656_amd as fa
     from paper_2608_18656_amd.inputs import Q8_LAYER_SHAPES, WORKLOADS, make_q8_0, make_workload
 
+    if what.startswith("paged_"):
+        w = WORKLOADS[what[len("paged_"):]]
+        ps = int(argv[2]) if len(argv) > 2 else 256
+        reps = int(argv[3]) if len(argv) > 3 else 5
+        q, k, v = make_workload(w)
+        npg = w.B * (w.Nk // ps)
+        perm = torch.randperm(npg, generator=torch.Generator().manual_seed(4000))
+        kp = torch.empty((npg, ps, w.Hkv, w.D), dtype=k.dtype)
+        vp = torch.empty_like(kp)
+        kp[perm] = k.reshape(npg, ps, w.Hkv, w.D)
+        vp[perm] = v.reshape(npg, ps, w.Hkv, w.D)
+        table = perm.reshape(w.B, -1).to(torch.int32).cuda()
+        sl = torch.full((w.B,), w.Nk, dtype=torch.int32, device="cuda")
+        qd, kp, vp = q.cuda(), kp.cuda(), vp.cuda()
+        for _ in range(reps):
+            fa.fwd_kvcache_paged(qd, kp, vp, table, sl, scale=w.softmax_scale)
+        torch.cuda.synchronize()
+        print(f"ran {what} pages of {ps} x {reps}", flush=True)
+        return
     reps = int(argv[2]) if len(argv) > 2 else 5
     if what.startswith("q8_"):
         shape = {n: (M, K) for n, M, K in Q8_LAYER_SHAPES}[what[3:]]
