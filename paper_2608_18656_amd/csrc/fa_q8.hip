@@ -5,8 +5,8 @@
 //
 // The product is bound by HBM: every weight byte (34 per 32 weights) is read
 // once, 2 flops per weight.  Each row is taken by L consecutive lanes of a
-// wave (R = 64 / L rows per wave at a time, L chosen so that the lanes of a
-// row have work).  When a row has an even number of blocks, every row and
+// wave (R = 64 / L rows per wave at a time; L of 16, 32 or 64, the one that
+// leaves the fewest lanes idle in a row's last round).  When a row has an even number of blocks, every row and
 // every pair of blocks (68 bytes) starts on a 4-byte boundary, and a lane's
 // unit of work is one pair: four 16-byte loads and one 4-byte load
 // (consecutive lanes take consecutive pairs, so a row streams contiguously).
@@ -362,9 +362,20 @@ hipError_t launch_q8_t(const void *w, const void *x, void *y, int M, int K, hipS
     a.units = PAIR ? K / 64 : K / 32;                   // lane work items per row
     a.L = 64;
     a.lgL = 6;
-    while (a.L > 16 && a.L / 2 >= a.units) {            // rows short of work share a wave
-        a.L /= 2;
-        --a.lgL;
+    {   // lanes per row: the fewest idle lanes in a row's last round (more
+        // lanes per row on ties); rows short of work share a wave
+        int best = 64, least = 1 << 30;
+        for (int Lc = 64; Lc >= 16; Lc /= 2) {
+            const int idle = (a.units + Lc - 1) / Lc * Lc - a.units;
+            if (idle < least) {
+                least = idle;
+                best = Lc;
+            }
+        }
+        while (a.L > best) {
+            a.L /= 2;
+            --a.lgL;
+        }
     }
     a.lgR = 6 - a.lgL;
     a.rounds = (a.units + a.L - 1) / a.L;
