@@ -2,9 +2,11 @@
 // kernels do not take: fp32 inputs, and fp16 / bf16 with a head dimension
 // other than 64 or 128 (any D with D % 8 == 0 and D <= 256).
 //
-// All arithmetic is fp32.  A workgroup of 256 threads owns 64 query rows of
-// one query head; four consecutive threads share a row and each holds an
-// interleaved quarter of its D columns (pairs d = 8 i + 2 t + {0, 1}).  Keys
+// All arithmetic is fp32.  A workgroup of 256 threads owns 256 / TPR query
+// rows of one query head; TPR consecutive threads share a row and each holds
+// an interleaved 1 / TPR of its D columns (pairs d = 2 TPR i + 2 t + {0, 1}).
+// TPR is 4 (64 rows per workgroup), or 16 (16 rows) when a grid of 64-row
+// workgroups would leave most CUs idle.  Keys
 // are streamed in LDS tiles (the next tile's loads in flight during the
 // current one); per tile the scores of all tile keys are formed
 // (partial dot products reduced over the four threads of the row), then the
@@ -23,7 +25,7 @@ struct GenericArgs {
     float *lse;
     int B, Hq, Hkv, Nq, Nk, D;
     float c;   // scale * log2(e), signed
-    int nmb;   // row blocks of 64
+    int nmb;   // row blocks (of 256 / TPR rows)
     const int *seqlens;   // valid keys per batch element (NULL: Nk for all)
 };
 
@@ -31,15 +33,17 @@ template <typename T> struct Scalar { typedef T type; };
 template <> struct Scalar<f16_t> { typedef _Float16 type; };
 template <> struct Scalar<bf16_t> { typedef __bf16 type; };
 
-template <typename TIN, typename TOUT, int DMAX, bool CAUSAL>
+template <typename TIN, typename TOUT, int DMAX, bool CAUSAL, int TPR>
 __global__ __launch_bounds__(256) void generic_kernel(GenericArgs a) {
     typedef typename Scalar<TIN>::type S;
     constexpr int KT = 16;                       // keys per LDS tile
-    constexpr int NP = DMAX / 8;                 // column pairs per thread
+    constexpr int RW = 256 / TPR;                // query rows per workgroup
+    constexpr int NP = DMAX / (2 * TPR);         // column pairs per thread
+    static_assert(NP >= 1, "at least one column pair per thread");
     __shared__ __attribute__((aligned(16))) float ks[KT * DMAX];
     __shared__ __attribute__((aligned(16))) float vs[KT * DMAX];
 
-    const int tid = threadIdx.x, row = tid >> 2, part = tid & 3;
+    const int tid = threadIdx.x, row = tid / TPR, part = tid % TPR;
     int bid = blockIdx.x;
     const int mb = a.nmb - 1 - bid % a.nmb;
     bid /= a.nmb;
@@ -49,9 +53,9 @@ __global__ __launch_bounds__(256) void generic_kernel(GenericArgs a) {
     const int D = a.D, Nq = a.Nq;
     // valid keys of this batch element (a.Nk rows per element in K and V)
     const int Nk = a.seqlens ? min(max(a.seqlens[b], 0), a.Nk) : a.Nk;
-    const int qi = mb * 64 + row;
+    const int qi = mb * RW + row;
     const int off = Nk - Nq;
-    const int last_blk = min(mb * 64 + 64, Nq) - 1;
+    const int last_blk = min(mb * RW + RW, Nq) - 1;
     const int kend = CAUSAL ? min(Nk, last_blk + off + 1) : Nk;
     const int myend = CAUSAL ? min(Nk, qi + off + 1) : Nk;
 
@@ -59,7 +63,7 @@ __global__ __launch_bounds__(256) void generic_kernel(GenericArgs a) {
     const S *qp = reinterpret_cast<const S *>(a.q) + ((size_t)((size_t)b * Nq + qi) * a.Hq + h) * D;
 #pragma unroll
     for (int i = 0; i < NP; ++i) {
-        const int d = 8 * i + 2 * part;
+        const int d = 2 * TPR * i + 2 * part;
         q0[i] = (qi < Nq && d < D) ? to_f32(qp[d]) : 0.f;
         q1[i] = (qi < Nq && d < D) ? to_f32(qp[d + 1]) : 0.f;
         o0[i] = 0.f;
@@ -120,11 +124,11 @@ __global__ __launch_bounds__(256) void generic_kernel(GenericArgs a) {
             float acc = 0.f;
 #pragma unroll
             for (int i = 0; i < NP; ++i) {
-                const int d = 8 * i + 2 * part;
+                const int d = 2 * TPR * i + 2 * part;
                 acc += q0[i] * ks[j * DMAX + d] + q1[i] * ks[j * DMAX + d + 1];
             }
-            acc += __shfl_xor(acc, 1);
-            acc += __shfl_xor(acc, 2);
+#pragma unroll
+            for (int off = 1; off < TPR; off <<= 1) acc += __shfl_xor(acc, off);
             const bool vis = kb + j < myend;
             x[j] = vis ? acc * a.c : -INFINITY;
             tmax = __builtin_fmaxf(tmax, x[j]);
@@ -145,7 +149,7 @@ __global__ __launch_bounds__(256) void generic_kernel(GenericArgs a) {
             lsum += p;
 #pragma unroll
             for (int i = 0; i < NP; ++i) {
-                const int d = 8 * i + 2 * part;
+                const int d = 2 * TPR * i + 2 * part;
                 o0[i] += p * vs[j * DMAX + d];
                 o1[i] += p * vs[j * DMAX + d + 1];
             }
@@ -156,7 +160,7 @@ __global__ __launch_bounds__(256) void generic_kernel(GenericArgs a) {
     TOUT *op = reinterpret_cast<TOUT *>(a.o) + ((size_t)((size_t)b * Nq + qi) * a.Hq + h) * D;
 #pragma unroll
     for (int i = 0; i < NP; ++i) {
-        const int d = 8 * i + 2 * part;
+        const int d = 2 * TPR * i + 2 * part;
         if (d < D) {
             op[d] = from_f32<TOUT>(o0[i] * inv);
             op[d + 1] = from_f32<TOUT>(o1[i] * inv);
@@ -173,15 +177,25 @@ hipError_t launch_t(const Problem &p, hipStream_t stream) {
     a.B = p.B; a.Hq = p.Hq; a.Hkv = p.Hkv; a.Nq = p.Nq; a.Nk = p.Nk; a.D = p.D;
     a.seqlens = p.seqlens;
     a.c = p.scale * kLog2e;
-    a.nmb = (p.Nq + 63) / 64;
+    // 16 threads per row (16-row workgroups) when 64-row workgroups would not
+    // give every CU of the GPU one
+    const bool narrow = (long long)((p.Nq + 63) / 64) * p.B * p.Hq < 256;
+    const int RW = narrow ? 16 : 64;
+    a.nmb = (p.Nq + RW - 1) / RW;
     const long long nblocks = (long long)a.nmb * p.B * p.Hq;
     if (nblocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-    if (p.causal)
-        hipLaunchKernelGGL((generic_kernel<TIN, TOUT, DMAX, true>), dim3((unsigned)nblocks),
-                           dim3(256), 0, stream, a);
-    else
-        hipLaunchKernelGGL((generic_kernel<TIN, TOUT, DMAX, false>), dim3((unsigned)nblocks),
-                           dim3(256), 0, stream, a);
+    const dim3 grid((unsigned)nblocks), block(256);
+    if (narrow) {
+        if (p.causal)
+            hipLaunchKernelGGL((generic_kernel<TIN, TOUT, DMAX, true, 16>), grid, block, 0, stream, a);
+        else
+            hipLaunchKernelGGL((generic_kernel<TIN, TOUT, DMAX, false, 16>), grid, block, 0, stream, a);
+    } else {
+        if (p.causal)
+            hipLaunchKernelGGL((generic_kernel<TIN, TOUT, DMAX, true, 4>), grid, block, 0, stream, a);
+        else
+            hipLaunchKernelGGL((generic_kernel<TIN, TOUT, DMAX, false, 4>), grid, block, 0, stream, a);
+    }
     return hipGetLastError();
 }
 
