@@ -223,7 +223,7 @@ __global__ __launch_bounds__(NT) void q8_gemv_kernel(const unsigned char *__rest
     const int wv = (int)blockIdx.x * WAVES + wave;          // this wave's index
     const int my_groups = wv < groups ? (int)((unsigned)(groups - 1 - wv) / (unsigned)NW) + 1 : 0;
     const int steps = my_groups * rounds;
-    const unsigned row_bytes = (unsigned)nb * 34u;           // R > 1 only for rows of <= 2176 bytes
+    const unsigned row_bytes = (unsigned)nb * 34u;           // R rows fit in 2^31 - 1 bytes (host)
     const long long group_bytes = (long long)R * row_bytes;
     float *xs = smem;
     float *ybuf = smem + (XM == X_LDS ? K + K / 16 : 0) + wave * Q8_YB;
@@ -363,9 +363,12 @@ hipError_t launch_q8_t(const void *w, const void *x, void *y, int M, int K, hipS
     a.L = 64;
     a.lgL = 6;
     {   // lanes per row: the fewest idle lanes in a row's last round (more
-        // lanes per row on ties); rows short of work share a wave
+        // lanes per row on ties); rows short of work share a wave, as long as
+        // the 64 / L rows of a group fit the 31-bit view a wave loads through
+        const long long row_bytes = (long long)(K / 32) * 34;
         int best = 64, least = 1 << 30;
         for (int Lc = 64; Lc >= 16; Lc /= 2) {
+            if ((64 / Lc) * row_bytes > 0x7fffffffLL) continue;
             const int idle = (a.units + Lc - 1) / Lc * Lc - a.units;
             if (idle < least) {
                 least = idle;
