@@ -164,3 +164,29 @@ def test_paged_argument_errors_before_any_launch():
     assert call(lse=S) == 8                        # lse overlaps the lengths
     assert call(o=K + 64) == 8                     # o inside the K pool (8 pages of 64 x 2 x 64 x 2 B)
     assert call(Hq=6, Hkv=4) == 3
+
+
+def test_header_is_plain_c(tmp_path):
+    """include/fa.h compiles as C11 (no C++ in the boundary) and declares
+    every entry point with the signature the library exports."""
+    import shutil
+    import subprocess
+
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    names = declared_functions()
+    src = tmp_path / "uses_fa.c"
+    body = "\n".join(f"    (void)&{n};" for n in names)
+    src.write_text(
+        '#include "fa.h"\n'
+        "int main(void) {\n"
+        f"{body}\n"
+        "    fa_status_t s = FA_OK; fa_dtype_t t = FA_BF16; (void)s; (void)t;\n"
+        "    return FA_MAX_SPLITS == 256 && FA_ERR_PACKING == 13 ? 0 : 1;\n"
+        "}\n")
+    out = tmp_path / "uses_fa.o"
+    r = subprocess.run([cc, "-std=c11", "-Wall", "-Werror", "-pedantic", "-I",
+                        os.path.join(ROOT, "include"), "-c", str(src), "-o", str(out)],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
