@@ -150,6 +150,37 @@ def run_workload(torch, fa, w, steps, warmup, kv_sets=1, num_splits=None, packin
     return ms, sets[0], outs[0], lses[0]
 
 
+def unfused_vs_fused(torch, fa, w, steps):
+    """Fused kernel against the unfused path on one workload.  The unfused
+    path's minimum HBM traffic: per visible score, S written (4 B) and read
+    (4 B) and P written (2 B) and read (2 B); Q, K, V and O once."""
+    from paper_2608_18656_amd.inputs import DTYPES, make_workload
+
+    q, k, v = (t.cuda() for t in make_workload(w))
+    out = torch.empty_like(q)
+    lse = torch.empty((w.B, w.Hq, w.Nq), dtype=torch.float32, device="cuda")
+    ws = torch.empty(fa.unfused_workspace_bytes(w.B, w.Hq, w.Nq, w.Nk), dtype=torch.uint8,
+                     device="cuda")
+    fused_ms = time_calls(torch, [lambda: fa.fwd(q, k, v, causal=w.causal, scale=w.softmax_scale,
+                                                 out=out, lse=lse)], steps, 2)
+    unf_ms = time_calls(torch, [lambda: fa.fwd_unfused(q, k, v, causal=w.causal,
+                                                       scale=w.softmax_scale, out=out, lse=lse,
+                                                       workspace=ws)], steps, 2)
+    es = torch.finfo(DTYPES[w.dtype]).bits // 8
+    vis = w.B * w.Hq * w.visible_pairs()
+    io = (2 * w.B * w.Nq * w.Hq * w.D + 2 * w.B * w.Nk * w.Hkv * w.D) * es
+    nbytes = 12 * vis + io
+    del ws
+    return {"workload": w.name, "fused_us": round(fused_ms * 1e3, 2),
+            "unfused_us": round(unf_ms * 1e3, 2), "fused_speedup": round(unf_ms / fused_ms, 2),
+            "fused_tflops": round(w.flops() / (fused_ms * 1e-3) / 1e12, 1),
+            "unfused_tflops": round(w.flops() / (unf_ms * 1e-3) / 1e12, 1),
+            "unfused_min_hbm_bytes": nbytes,
+            "unfused_gbs": round(nbytes / (unf_ms * 1e-3) / 1e9, 1),
+            "unfused_frac_hbm": round(nbytes / (unf_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+            "steps": steps}
+
+
 def cpu_baseline(w, q_cpu_dev, o_dev, lse_dev):
     """The oracle as it stands, on the host cores, over the whole workload;
     also the max error of the benchmark's GPU output against it."""
@@ -329,7 +360,7 @@ def main():
     ap.add_argument("--no-sclk", action="store_true",
                     help="skip the shader-clock reading under load (a burst of headline calls)")
     ap.add_argument("--no-ablation", action="store_true",
-                    help="skip the inter-head packing ablation (e.g. under a kernel trace)")
+                    help="skip the inter-head packing and unfused ablations (e.g. under a kernel trace)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -443,6 +474,21 @@ def main():
                 f"{row['per_head_us']} us ({row['speedup']}x)")
         if ablation:
             result["packing_ablation"] = ablation
+        # fused against unfused self-attention (score matrix S in fp32 and
+        # weights P in fp16 through HBM), the comparison of the paper's
+        # evaluation of its optimised self-attention
+        unfused = []
+        for name in (() if args.no_ablation else
+                     ("gqa_prefill_bf16", "gqa_prefill_d128_f16", "mqa_prefill_f16")):
+            x = WORKLOADS[name]
+            steps = max(3, min(args.steps, 10))
+            row = unfused_vs_fused(torch, fa, x, steps)
+            unfused.append(row)
+            log(f"[bench] unfused {name}: {row['unfused_us']} us against fused {row['fused_us']} us "
+                f"({row['fused_speedup']}x); S/P traffic {row['unfused_gbs']} GB/s")
+            torch.cuda.empty_cache()
+        if unfused:
+            result["unfused_ablation"] = unfused
         # decode against a paged K/V cache (pages of 64 and 256 keys, shuffled)
         xw = WORKLOADS["gqa_decode_bf16"]
         paged = {"workload": xw.name, "metric": "decode KV GB/s, K/V in shuffled pages", "pages": []}

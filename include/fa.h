@@ -207,6 +207,35 @@ fa_status_t fa_release_workspace(void);
  * misaligned pointer, FA_ERR_HIP when the current device cannot be read. */
 fa_status_t fa_set_workspace(void *dev_ptr, size_t bytes);
 
+/* Unfused self-attention: the same result as fa_fwd, computed the way the
+ * paper's optimised self-attention does it (Sec. 4.2), with the score matrix
+ * materialised -- the comparison point of its fused kernel (Sec. 6.2).  Three
+ * kernels run in order on `stream`, each leaving its result in the workspace:
+ * S = scale * Q K^T (fp32), P = the row-wise softmax of S (fp16, normalised;
+ * lse from the fp32 maximum and sum), O = P V (fp32 accumulation, one
+ * rounding to out_dtype).  GQA/MQA heads share K and V as in fa_fwd; causal
+ * is bottom-right aligned; score tiles past the causal edge are not computed.
+ *   workspace  device, 256-byte aligned, at least
+ *              fa_unfused_workspace_bytes(B, Hq, Nq, Nk) bytes, owned by the
+ *              caller; scratch only (its contents after the call are the
+ *              scores [B][Hq][Nq][NkP] fp32 followed by the weights
+ *              [B][Hq][Nq][NkP] fp16, NkP = Nk rounded up to 64, defined on
+ *              each row's visible keys).  Calls sharing one workspace must be
+ *              ordered.
+ * fp16 / bf16 inputs with D in {64, 128} only.  Errors: those of fa_fwd, then
+ * FA_ERR_DTYPE for fp32 inputs, FA_ERR_HEAD_DIM for another D, FA_ERR_NULL
+ * for a NULL workspace, FA_ERR_ALIGN for a misaligned one, FA_ERR_DIM when
+ * the workspace size overflows, FA_ERR_WORKSPACE when workspace_bytes is too
+ * small, FA_ERR_ALIAS when it overlaps a tensor; all before any HIP call. */
+fa_status_t fa_fwd_unfused(const void *q, const void *k, const void *v, void *o, float *lse,
+                           int B, int Hq, int Hkv, int Nq, int Nk, int D, int causal,
+                           float scale, void *stream, fa_dtype_t in_dtype,
+                           fa_dtype_t out_dtype, void *workspace, size_t workspace_bytes);
+
+/* Bytes of workspace fa_fwd_unfused needs: 6 * B * Hq * Nq * NkP (0 when a
+ * size is < 1 or the product overflows). */
+size_t fa_unfused_workspace_bytes(int B, int Hq, int Nq, int Nk);
+
 /* Q8_0 matrix-vector product y = W x, the form the linear projection and
  * feed-forward layers take in decode, where a single token is processed
  * (Sec. 4.3).  W (M x K, row-major) is in the 8-bit block format Q8_0 of

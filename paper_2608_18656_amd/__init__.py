@@ -8,7 +8,8 @@ from __future__ import annotations
 
 import math
 
-__all__ = ["fwd", "fwd_splitkv", "fwd_kvcache", "fwd_kvcache_paged", "q8_0_gemv", "FaError", "validate", "workspace_bytes", "release_workspace",
+__all__ = ["fwd", "fwd_splitkv", "fwd_kvcache", "fwd_kvcache_paged", "fwd_unfused",
+           "unfused_workspace_bytes", "q8_0_gemv", "FaError", "validate", "workspace_bytes", "release_workspace",
            "set_workspace", "version", "DTYPE_CODES"]
 
 
@@ -105,6 +106,48 @@ def fwd(q, k, v, causal: bool = False, scale: float | None = None, out=None, lse
             st = lib.fa_fwd_packed(*args, int(heads_per_workgroup))
         else:
             st = lib.fa_fwd(*args)
+    _check(lib, st)
+    return out, lse
+
+
+def unfused_workspace_bytes(B: int, Hq: int, Nq: int, Nk: int) -> int:
+    """Workspace bytes of fwd_unfused (fa_unfused_workspace_bytes)."""
+    from . import _lib
+
+    return int(_lib.load().fa_unfused_workspace_bytes(B, Hq, Nq, Nk))
+
+
+def fwd_unfused(q, k, v, causal: bool = False, scale: float | None = None, out=None, lse=None,
+                out_dtype=None, return_lse: bool = True, workspace=None):
+    """Unfused self-attention (fa_fwd_unfused): the result of ``fwd`` with the
+    score matrix materialised -- S = scale q k^T in fp32, P = softmax(S) in
+    fp16, then O = P v, three kernels through HBM.  fp16 / bf16, D in {64,
+    128}.  ``workspace``: a contiguous uint8 GPU tensor of at least
+    unfused_workspace_bytes(B, Hq, Nq, Nk) bytes (allocated per call when
+    None); afterwards it holds S [B, Hq, Nq, NkP] fp32 followed by P
+    [B, Hq, Nq, NkP] fp16 (NkP = Nk rounded up to 64) on each row's visible
+    keys.  Returns (out, lse) as ``fwd``.
+    """
+    from . import _lib
+
+    lib = _lib.load()
+    torch = _torch()
+    (B, Hq, Hkv, Nq, Nk, D), out, lse, odt = _prepare(q, k, v, out, lse, out_dtype, return_lse)
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    need = int(lib.fa_unfused_workspace_bytes(B, Hq, Nq, Nk))
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+    elif (workspace.dtype != torch.uint8 or not workspace.is_contiguous()
+          or workspace.device != q.device):
+        raise ValueError("workspace must be a contiguous uint8 tensor on q's device")
+    codes = _codes()
+    stream = torch.cuda.current_stream(q.device).cuda_stream
+    with torch.cuda.device(q.device):
+        st = lib.fa_fwd_unfused(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                                lse.data_ptr() if lse is not None else None, B, Hq, Hkv, Nq, Nk,
+                                D, int(bool(causal)), float(scale), stream, codes[q.dtype],
+                                codes.get(odt, -1), workspace.data_ptr(), workspace.numel())
     _check(lib, st)
     return out, lse
 

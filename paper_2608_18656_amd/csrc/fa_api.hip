@@ -1,5 +1,5 @@
 // fa_api.hip -- the exported C entry points: argument validation, dispatch to
-// the prefill / decode / generic kernels, and the decode workspace.
+// the prefill / decode / generic / unfused kernels, and the decode workspace.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -312,6 +312,36 @@ fa_status_t fa_q8_0_gemv(const void *w, const void *x, void *y, int M, int K, fa
         return FA_ERR_ALIAS;
     const hipError_t e =
         fa::launch_q8_gemv(w, x, y, M, K, x_dtype, y_dtype, reinterpret_cast<hipStream_t>(stream));
+    return e == hipSuccess ? FA_OK : FA_ERR_HIP;
+}
+
+size_t fa_unfused_workspace_bytes(int B, int Hq, int Nq, int Nk) {
+    return fa::unfused_workspace_bytes(B, Hq, Nq, Nk);
+}
+
+fa_status_t fa_fwd_unfused(const void *q, const void *k, const void *v, void *o, float *lse, int B,
+                           int Hq, int Hkv, int Nq, int Nk, int D, int causal, float scale,
+                           void *stream, fa_dtype_t in_dtype, fa_dtype_t out_dtype,
+                           void *workspace, size_t workspace_bytes) {
+    fa_status_t st = validate_core(q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, in_dtype,
+                                   out_dtype, -1);
+    if (st != FA_OK) return st;
+    if (in_dtype == FA_F32) return FA_ERR_DTYPE;
+    if (!fa::unfused_supported(D, in_dtype)) return FA_ERR_HEAD_DIM;
+    if (!workspace) return FA_ERR_NULL;
+    if (reinterpret_cast<uintptr_t>(workspace) & 255) return FA_ERR_ALIGN;
+    const size_t need = fa::unfused_workspace_bytes(B, Hq, Nq, Nk);
+    if (need == 0) return FA_ERR_DIM;
+    if (workspace_bytes < need) return FA_ERR_WORKSPACE;
+    const size_t qb = (size_t)B * Nq * Hq * D * esize(in_dtype), kb = (size_t)B * Nk * Hkv * D * esize(in_dtype);
+    const size_t ob = (size_t)B * Nq * Hq * D * esize(out_dtype), lb = (size_t)B * Hq * Nq * sizeof(float);
+    if (overlaps(workspace, need, q, qb) || overlaps(workspace, need, k, kb) ||
+        overlaps(workspace, need, v, kb) || overlaps(workspace, need, o, ob) ||
+        (lse && overlaps(workspace, need, lse, lb)))
+        return FA_ERR_ALIAS;
+    fa::Problem p{q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, in_dtype, out_dtype, 0,
+                  nullptr, nullptr, 0, 0, 0};
+    const hipError_t e = fa::launch_unfused(p, workspace, reinterpret_cast<hipStream_t>(stream));
     return e == hipSuccess ? FA_OK : FA_ERR_HIP;
 }
 

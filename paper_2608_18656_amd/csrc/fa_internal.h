@@ -31,6 +31,7 @@ struct Problem {
 hipError_t launch_prefill(const Problem &p, hipStream_t stream);
 hipError_t launch_generic(const Problem &p, hipStream_t stream);
 hipError_t launch_decode(const Problem &p, int splits, void *workspace, hipStream_t stream);
+hipError_t launch_unfused(const Problem &p, void *workspace, hipStream_t stream);
 hipError_t launch_q8_gemv(const void *w, const void *x, void *y, int M, int K, fa_dtype_t x_dtype,
                           fa_dtype_t y_dtype, hipStream_t stream);
 
@@ -39,5 +40,10 @@ bool decode_supported(int Nq, int D, fa_dtype_t in);
 bool prefill_supported(int D, fa_dtype_t in);
 int decode_default_splits(int B, int Hq, int Hkv, int Nk, int D);
 size_t decode_workspace_bytes(int B, int Hq, int D, int splits);
+
+// Unfused path: supported shapes and the workspace it needs (0 when a size is
+// < 1 or the product overflows).
+bool unfused_supported(int D, fa_dtype_t in);
+size_t unfused_workspace_bytes(long long B, long long Hq, long long Nq, long long Nk);
 
 }  // namespace fa

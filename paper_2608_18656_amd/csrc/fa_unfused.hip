@@ -1,0 +1,360 @@
+// fa_unfused.hip -- unfused self-attention forward on gfx950: the path with a
+// materialised score matrix that the paper optimises beside FlashAttention-V
+// (Sec. 4.2) and measures it against (Sec. 6.2, self-attention against the
+// fused kernel in prefill).  Three kernels, each leaving its whole result in
+// HBM for the next:
+//   scores   S = scale * Q K^T in fp32, [B][Hq][Nq][NkP] (NkP = Nk rounded up
+//            to 64 keys); masked entries are -inf.  A workgroup's four waves
+//            are four (query head, 32-row block) slots that read one
+//            key/value head -- query heads of one group at the same rows when
+//            the group size allows, the reuse across heads of Sec. 4.2 (one
+//            staged key row serves several heads) -- and it takes a chunk of
+//            64-key tiles; tiles past the causal edge are not computed.
+//            32x32x16 MFMA, A = the wave's 32 query rows (registers),
+//            B = 32 key rows of the tile in LDS.
+//   softmax  one wave per query row: the running maximum and sum over the
+//            visible keys (first pass), then P = 2^(S log2 e - max) / sum in
+//            fp16 (second pass) with zeros from the last visible key up to
+//            the end of the last tile the P.V kernel reads for that row, and
+//            the row's log-sum-exp.
+//   pv       O = P V.  A = 16 keys of P per lane, read straight from HBM;
+//            B = V from a row-major fp16 copy of the 64-key tile in LDS, read
+//            with the transposing LDS load (four keys of one column per
+//            read); fp32 accumulation, one rounding to the output type.
+// The score matrix costs 4 bytes written and up to 8 read per visible score,
+// and P 2 written and 2 read: the traffic the fused kernel never makes.
+#include "fa_common.h"
+#include "fa_internal.h"
+
+namespace fa {
+namespace {
+
+constexpr int UR = 32;       // query rows per slot (one wave)
+constexpr int USLOT = 4;     // slots per workgroup
+constexpr int UKT = 64;      // keys per tile
+constexpr int UCHUNK = 8;    // key tiles per scores workgroup
+constexpr int UNT = 64 * USLOT;
+
+struct UnfusedArgs {
+    const void *q, *k, *v;
+    void *o;
+    float *lse;
+    float *s;           // workspace: scores, [B][Hq][Nq][NkP] fp32
+    _Float16 *p;        // workspace: weights, [B][Hq][Nq][NkP] fp16
+    int B, Hq, Hkv, Nq, Nk, NkP;
+    float scale;
+    int HW;             // query heads per workgroup (4, 2 or 1)
+    int nmb;            // row blocks of 32 * (4 / HW) rows
+    int nhg;            // head groups per key/value head (G / HW)
+    int nchunk;         // key-tile chunks per row block (scores)
+};
+
+// Slot of wave w of a workgroup whose row block is mb, head group hg, key/value head g.
+struct Slot {
+    int h, row0, row0_wg, rows_wg;
+};
+__device__ __forceinline__ Slot slot_of(const UnfusedArgs &a, int w, int mb, int hg, int g) {
+    const int G = a.Hq / a.Hkv, RB = USLOT / a.HW;
+    Slot s;
+    s.h = g * G + hg * a.HW + w % a.HW;
+    s.rows_wg = UR * RB;
+    s.row0_wg = mb * s.rows_wg;
+    s.row0 = s.row0_wg + (w / a.HW) * UR;
+    return s;
+}
+
+// Visible keys of query row i (bottom-right causal alignment).
+__device__ __forceinline__ int kend_row(int i, int Nq, int Nk, bool causal) {
+    return causal ? min(Nk, i + Nk - Nq + 1) : Nk;
+}
+
+// Copy of one 64-key tile of K or V (keys t0 .. t0 + 63 of head g) into
+// registers: chunk c = tid + 256 i is key c / (D / 8), columns 8 (c % (D / 8)).
+// Keys past Nk read as zero.
+template <typename TIN, int D>
+__device__ __forceinline__ void tile_load(const void *base, int b, int g, int Hkv, int Nk, int t0,
+                                          int tid, uint4_t (&r)[UKT * D / 8 / UNT]) {
+    using S = typename TIN::scalar;
+    constexpr int CPR = D / 8;
+#pragma unroll
+    for (int i = 0; i < UKT * CPR / UNT; ++i) {
+        const int c = tid + UNT * i;
+        const int key = t0 + c / CPR;
+        r[i] = uint4_t{0u, 0u, 0u, 0u};
+        if (key < Nk)
+            r[i] = ld16(reinterpret_cast<const S *>(base) +
+                        ((size_t)((size_t)b * Nk + key) * Hkv + g) * D + 8 * (c % CPR));
+    }
+}
+
+template <typename TIN, int D, bool CAUSAL>
+__global__ __launch_bounds__(UNT) void unfused_scores_kernel(UnfusedArgs a) {
+    using S = typename TIN::scalar;
+    using V8 = typename TIN::vec8;
+    constexpr int KS = D + 8;            // LDS row stride (16-bit elements)
+    constexpr int KSTEPS = D / 16;
+    constexpr int CPR = D / 8;
+    constexpr int NLD = UKT * CPR / UNT;
+    __shared__ __attribute__((aligned(16))) unsigned short kt[UKT * KS];
+
+    const int tid = threadIdx.x;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int l = tid & 63, lq = l & 31, lh = l >> 5;
+    int bid = blockIdx.x;
+    const int chunk = bid % a.nchunk;
+    bid /= a.nchunk;
+    const int hg = bid % a.nhg;
+    bid /= a.nhg;
+    const int g = bid % a.Hkv;
+    bid /= a.Hkv;
+    const int b = bid % a.B;
+    const int mb = bid / a.B;
+    const Slot sl = slot_of(a, w, mb, hg, g);
+    const int Nq = a.Nq, Nk = a.Nk, off = Nk - Nq;
+
+    const int last_wg = min(sl.row0_wg + sl.rows_wg, Nq) - 1;
+    const int ntiles = (kend_row(last_wg, Nq, Nk, CAUSAL) + UKT - 1) / UKT;
+    const int t0 = chunk * UCHUNK, t1 = min(t0 + UCHUNK, ntiles);
+    if (t0 >= t1) return;   // the same for the whole workgroup
+    const bool live = sl.row0 < Nq;
+    const int kend_w = live ? kend_row(min(sl.row0 + UR, Nq) - 1, Nq, Nk, CAUSAL) : 0;
+
+    V8 qf[KSTEPS];
+    {
+        const int qrow = min(sl.row0 + lq, Nq - 1);
+        const S *qp = reinterpret_cast<const S *>(a.q) + ((size_t)((size_t)b * Nq + qrow) * a.Hq + sl.h) * D + 8 * lh;
+#pragma unroll
+        for (int ks = 0; ks < KSTEPS; ++ks) qf[ks] = as_vec8<V8>(ld16(qp + 16 * ks));
+    }
+    float *srow = a.s + ((size_t)((size_t)b * a.Hq + sl.h) * Nq) * a.NkP;
+
+    uint4_t kr[NLD];
+    tile_load<TIN, D>(a.k, b, g, a.Hkv, Nk, t0 * UKT, tid, kr);
+    for (int t = t0; t < t1; ++t) {
+        __syncthreads();   // the previous tile's operand reads are done
+#pragma unroll
+        for (int i = 0; i < NLD; ++i) {
+            const int c = tid + UNT * i;
+            st16(kt + (c / CPR) * KS + 8 * (c % CPR), kr[i]);
+        }
+        __syncthreads();
+        if (t + 1 < t1) tile_load<TIN, D>(a.k, b, g, a.Hkv, Nk, (t + 1) * UKT, tid, kr);
+        if (t * UKT >= kend_w) continue;   // wave-uniform: no row of the slot sees this tile
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+            float16_t s = float16_t{};
+#pragma unroll
+            for (int ks = 0; ks < KSTEPS; ++ks)
+                s = mfma32(qf[ks], as_vec8<V8>(*reinterpret_cast<const uint4_t *>(kt + (32 * half + lq) * KS + 8 * lh + 16 * ks)), s);
+            // lane l holds key (l % 32) of rows 8 (r / 4) + 4 (l / 32) + r % 4
+            const int key = t * UKT + 32 * half + lq;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int row = sl.row0 + 8 * (r >> 2) + 4 * lh + (r & 3);
+                if (row < Nq) {
+                    const bool vis = key < Nk && (!CAUSAL || key <= row + off);
+                    srow[(size_t)row * a.NkP + key] = vis ? s[r] * a.scale : -INFINITY;
+                }
+            }
+        }
+    }
+}
+
+// Maximum and sum pair of two lanes' partial states (log2 domain).
+__device__ __forceinline__ void lse_combine(float &m, float &sum, float m2, float s2) {
+    const float M = __builtin_fmaxf(m, m2);
+    const float a = (m == -INFINITY) ? 0.f : sum * exp2_fast(m - M);
+    const float b = (m2 == -INFINITY) ? 0.f : s2 * exp2_fast(m2 - M);
+    m = M;
+    sum = a + b;
+}
+
+template <bool CAUSAL>
+__global__ __launch_bounds__(UNT) void unfused_softmax_kernel(UnfusedArgs a) {
+    const int tid = threadIdx.x, l = tid & 63;
+    const long long row = (long long)blockIdx.x * USLOT + (tid >> 6);
+    if (row >= (long long)a.B * a.Hq * a.Nq) return;   // no barrier below
+    const int i = (int)(row % a.Nq);
+    const int kend = kend_row(i, a.Nq, a.Nk, CAUSAL);
+    // the P.V kernel reads whole 64-key tiles up to the extent of the last
+    // row of this row's 32-row slot, at most 31 keys past this row's own
+    const int zend = min(a.NkP, ((kend + UKT - 1) / UKT) * UKT + UKT);
+    const float *sr = a.s + (size_t)row * a.NkP;
+    _Float16 *pr = a.p + (size_t)row * a.NkP;
+
+    float m = -INFINITY, sum = 0.f;
+    for (int c = 4 * l; c < kend; c += 256) {
+        const float4_t x = *reinterpret_cast<const float4_t *>(sr + c);
+        float t[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) t[e] = (c + e < kend) ? x[e] * kLog2e : -INFINITY;
+        const float mx = __builtin_fmaxf(__builtin_fmaxf(t[0], t[1]), __builtin_fmaxf(t[2], t[3]));
+        if (mx > m) {
+            sum = (m == -INFINITY) ? 0.f : sum * exp2_fast(m - mx);
+            m = mx;
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sum += exp2_fast(t[e] - m);
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        const float m2 = __shfl_xor(m, o), s2 = __shfl_xor(sum, o);
+        lse_combine(m, sum, m2, s2);
+    }
+    const float inv = 1.f / sum;
+    if (a.lse && l == 0) a.lse[row] = (m + __builtin_log2f(sum)) * kLn2;
+    for (int c = 4 * l; c < zend; c += 256) {
+        half4_t out = {(_Float16)0.f, (_Float16)0.f, (_Float16)0.f, (_Float16)0.f};
+        if (c < kend) {
+            const float4_t x = *reinterpret_cast<const float4_t *>(sr + c);
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                out[e] = (c + e < kend) ? (_Float16)(exp2_fast(x[e] * kLog2e - m) * inv) : (_Float16)0.f;
+        }
+        *reinterpret_cast<half4_t *>(pr + c) = out;
+    }
+}
+
+template <typename TIN, typename TOUT, int D, bool CAUSAL>
+__global__ __launch_bounds__(UNT) void unfused_pv_kernel(UnfusedArgs a) {
+    constexpr int VS = D + 8;            // LDS row stride (fp16 elements)
+    constexpr int CPR = D / 8;
+    constexpr int NLD = UKT * CPR / UNT;
+    constexpr int DT = D / 32;
+    constexpr bool IN_BF16 = __is_same(TIN, bf16_t);
+    __shared__ __attribute__((aligned(16))) _Float16 vt[UKT * VS];
+
+    const int tid = threadIdx.x;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int l = tid & 63, lq = l & 31, lh = l >> 5;
+    int bid = blockIdx.x;
+    const int hg = bid % a.nhg;
+    bid /= a.nhg;
+    const int g = bid % a.Hkv;
+    bid /= a.Hkv;
+    const int b = bid % a.B;
+    const int mb = bid / a.B;
+    const Slot sl = slot_of(a, w, mb, hg, g);
+    const int Nq = a.Nq, Nk = a.Nk;
+
+    const int last_wg = min(sl.row0_wg + sl.rows_wg, Nq) - 1;
+    const int ntiles = (kend_row(last_wg, Nq, Nk, CAUSAL) + UKT - 1) / UKT;
+    const bool live = sl.row0 < Nq;
+    const int kend_w = live ? kend_row(min(sl.row0 + UR, Nq) - 1, Nq, Nk, CAUSAL) : 0;
+    const int ntiles_w = (kend_w + UKT - 1) / UKT;
+
+    // A operand source: 8 weights of row (row0 + l % 32) at keys 8 (l / 32) + 16 kk
+    const _Float16 *prow = a.p + ((size_t)((size_t)b * a.Hq + sl.h) * Nq + min(sl.row0 + lq, Nq - 1)) * a.NkP + 8 * lh;
+    // B operand: the transposing read gives lane j of each 16-lane group
+    // column c0 + j of four consecutive keys; lane j addresses key (r0 + j / 4),
+    // columns c0 + 4 (j % 4) .. + 3
+    const int j = l & 15;
+    const int vlane = (8 * lh + j / 4) * VS + 16 * ((l >> 4) & 1) + 4 * (j % 4);
+
+    float16_t oacc[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) oacc[dt] = float16_t{};
+    uint4_t vr[NLD];
+    if (ntiles > 0) tile_load<TIN, D>(a.v, b, g, a.Hkv, Nk, 0, tid, vr);
+    for (int t = 0; t < ntiles; ++t) {
+        const bool comp = t < ntiles_w;   // wave-uniform
+        half8_t pa[4];
+        if (comp) {
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) pa[kk] = as_vec8<half8_t>(ld16(prow + t * UKT + 16 * kk));
+        }
+        __syncthreads();   // the previous tile's operand reads are done
+#pragma unroll
+        for (int i = 0; i < NLD; ++i) {
+            const int c = tid + UNT * i;
+            st16(vt + (c / CPR) * VS + 8 * (c % CPR), IN_BF16 ? bf16x8_to_f16x8(vr[i]) : vr[i]);
+        }
+        __syncthreads();
+        if (t + 1 < ntiles) tile_load<TIN, D>(a.v, b, g, a.Hkv, Nk, (t + 1) * UKT, tid, vr);
+        if (!comp) continue;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+                const _Float16 *src = vt + vlane + 16 * kk * VS + 32 * dt;
+                const half8_t vb = cat_half8(lds_read_tr16(src), lds_read_tr16(src + 4 * VS));
+                oacc[dt] = mfma32(pa[kk], vb, oacc[dt]);
+            }
+        }
+    }
+    if (!live) return;
+    // lane l holds column 32 dt + l % 32 of rows 8 (r / 4) + 4 (l / 32) + r % 4
+    TOUT *o = reinterpret_cast<TOUT *>(a.o);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        const int row = sl.row0 + 8 * (r >> 2) + 4 * lh + (r & 3);
+        if (row < Nq) {
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt)
+                o[((size_t)((size_t)b * Nq + row) * a.Hq + sl.h) * D + 32 * dt + lq] = from_f32<TOUT>(oacc[dt][r]);
+        }
+    }
+}
+
+template <typename TIN, typename TOUT, int D, bool CAUSAL>
+hipError_t launch_t(const UnfusedArgs &a, hipStream_t s) {
+    const long long per = (long long)a.nmb * a.B * a.Hkv * a.nhg;
+    const long long nsc = per * a.nchunk;
+    const long long nrow = ((long long)a.B * a.Hq * a.Nq + USLOT - 1) / USLOT;
+    if (nsc > 0x7fffffffLL || nrow > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL((unfused_scores_kernel<TIN, D, CAUSAL>), dim3((unsigned)nsc), dim3(UNT), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((unfused_softmax_kernel<CAUSAL>), dim3((unsigned)nrow), dim3(UNT), 0, s, a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((unfused_pv_kernel<TIN, TOUT, D, CAUSAL>), dim3((unsigned)per), dim3(UNT), 0, s, a);
+    return hipGetLastError();
+}
+
+template <typename TIN, typename TOUT>
+hipError_t launch_d(const Problem &p, const UnfusedArgs &a, hipStream_t s) {
+    if (p.D == 64)
+        return p.causal ? launch_t<TIN, TOUT, 64, true>(a, s) : launch_t<TIN, TOUT, 64, false>(a, s);
+    return p.causal ? launch_t<TIN, TOUT, 128, true>(a, s) : launch_t<TIN, TOUT, 128, false>(a, s);
+}
+
+}  // namespace
+
+size_t unfused_workspace_bytes(long long B, long long Hq, long long Nq, long long Nk) {
+    if (B < 1 || Hq < 1 || Nq < 1 || Nk < 1) return 0;
+    const long long nkp = (Nk + UKT - 1) / UKT * UKT;
+    const long long lim = 0x7fffffffffffffffLL / 8;
+    if (B > lim / Hq) return 0;
+    const long long bh = B * Hq;
+    if (bh > lim / Nq) return 0;
+    const long long rows = bh * Nq;
+    if (rows > lim / nkp) return 0;
+    const long long n = rows * nkp;
+    if (n > lim / 6) return 0;
+    return (size_t)(n * 6);   // fp32 scores, then fp16 weights
+}
+
+bool unfused_supported(int D, fa_dtype_t in) { return (D == 64 || D == 128) && in != FA_F32; }
+
+hipError_t launch_unfused(const Problem &p, void *workspace, hipStream_t stream) {
+    UnfusedArgs a;
+    a.q = p.q; a.k = p.k; a.v = p.v; a.o = p.o; a.lse = p.lse;
+    a.B = p.B; a.Hq = p.Hq; a.Hkv = p.Hkv; a.Nq = p.Nq; a.Nk = p.Nk;
+    a.NkP = (p.Nk + UKT - 1) / UKT * UKT;
+    a.s = reinterpret_cast<float *>(workspace);
+    a.p = reinterpret_cast<_Float16 *>(reinterpret_cast<char *>(workspace) +
+                                       (size_t)p.B * p.Hq * p.Nq * a.NkP * sizeof(float));
+    a.scale = p.scale;
+    const int G = p.Hq / p.Hkv;
+    a.HW = G % 4 == 0 ? 4 : (G % 2 == 0 ? 2 : 1);
+    const int rows_wg = UR * (USLOT / a.HW);
+    a.nmb = (p.Nq + rows_wg - 1) / rows_wg;
+    a.nhg = G / a.HW;
+    a.nchunk = (a.NkP / UKT + UCHUNK - 1) / UCHUNK;
+    if (p.in == FA_BF16)
+        return p.out == FA_F32 ? launch_d<bf16_t, float>(p, a, stream) : launch_d<bf16_t, __bf16>(p, a, stream);
+    return p.out == FA_F32 ? launch_d<f16_t, float>(p, a, stream) : launch_d<f16_t, _Float16>(p, a, stream);
+}
+
+}  // namespace fa

@@ -12,6 +12,11 @@ projection (qkv, o, gate_up or down; bf16 activations); ``paged_<workload>
 of that size in a seeded random order.
 
     python3 paper_2608_18656_amd/profile_run.py paged_gqa_decode_bf16 256 5
+
+``unfused_<workload>`` runs the unfused self-attention path (scores,
+softmax and P.V kernels through a workspace) on a prefill workload.
+
+    python3 paper_2608_18656_amd/profile_run.py unfused_gqa_prefill_bf16 5
 """
 from __future__ import annotations
 
@@ -66,6 +71,16 @@ def main(argv):
             fa.q8_0_gemv(w, x)
         torch.cuda.synchronize()
         print(f"ran {what} {shape} x {reps}", flush=True)
+        return
+    if what.startswith("unfused_"):
+        w = WORKLOADS[what[len("unfused_"):]]
+        q, k, v = (t.cuda() for t in make_workload(w))
+        ws = torch.empty(fa.unfused_workspace_bytes(w.B, w.Hq, w.Nq, w.Nk), dtype=torch.uint8,
+                         device="cuda")
+        for _ in range(reps):
+            fa.fwd_unfused(q, k, v, causal=w.causal, scale=w.softmax_scale, workspace=ws)
+        torch.cuda.synchronize()
+        print(f"ran {what} x {reps}", flush=True)
         return
     w = WORKLOADS[what]
     q, k, v = (t.cuda() for t in make_workload(w))

@@ -190,3 +190,33 @@ def test_header_is_plain_c(tmp_path):
                         os.path.join(ROOT, "include"), "-c", str(src), "-o", str(out)],
                        capture_output=True, text=True)
     assert r.returncode == 0, r.stderr
+
+
+def test_unfused_argument_errors_before_any_launch():
+    """fa_fwd_unfused's own checks and fa_unfused_workspace_bytes (fake
+    addresses, no HIP call)."""
+    lib = _lib.load()
+    Q, K, V, O, L, W = (k << 32 for k in (1, 2, 3, 4, 5, 6))
+    F16, BF16, F32 = _lib.FA_F16, _lib.FA_BF16, _lib.FA_F32
+    need = lib.fa_unfused_workspace_bytes(2, 8, 100, 130)
+    assert need == 6 * 2 * 8 * 100 * 192                       # Nk rounded up to 64
+    assert lib.fa_unfused_workspace_bytes(1, 1, 1, 1) == 6 * 64
+    assert lib.fa_unfused_workspace_bytes(1, 1, 1, 64) == 6 * 64
+    assert lib.fa_unfused_workspace_bytes(0, 8, 100, 130) == 0
+    assert lib.fa_unfused_workspace_bytes(1, 8, -1, 130) == 0
+    assert lib.fa_unfused_workspace_bytes(1 << 30, 1 << 30, 1 << 30, 1 << 30) == 0   # overflow
+
+    def call(q=Q, k=K, v=V, o=O, lse=L, B=2, Hq=8, Hkv=2, Nq=100, Nk=130, D=64, causal=1,
+             scale=0.125, it=F16, ot=F16, ws=W, wsb=None):
+        return lib.fa_fwd_unfused(q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, None, it, ot,
+                                  ws, need if wsb is None else wsb)
+
+    assert call(q=None) == 1 and call(ws=None) == 1
+    assert call(Hq=6, Hkv=4) == 3 and call(Nq=200) == 5 and call(scale=float("nan")) == 6
+    assert call(it=F32, ot=F32) == 9 and call(ot=BF16) == 9
+    assert call(D=96) == 4 and call(D=32) == 4
+    assert call(ws=W + 128) == 7                          # workspace not 256-byte aligned
+    assert call(wsb=need - 1) == 10                       # workspace too small
+    assert call(ws=Q) == 8                                 # workspace over q
+    assert call(ws=O - 256) == 8                           # workspace runs into o
+    assert call(o=Q + 64) == 8                             # the checks of fa_fwd come first
