@@ -12,17 +12,20 @@
 //            64-key tiles; tiles past the causal edge are not computed.
 //            32x32x16 MFMA, A = the wave's 32 query rows (registers),
 //            B = 32 key rows of the tile in LDS.
-//   softmax  one wave per query row: the running maximum and sum over the
-//            visible keys (first pass), then P = 2^(S log2 e - max) / sum in
-//            fp16 (second pass) with zeros from the last visible key up to
-//            the end of the last tile the P.V kernel reads for that row, and
-//            the row's log-sum-exp.
+//   softmax  one wave per query row: the row's scores are read once into
+//            registers (the first 4096 keys; longer rows stream the rest
+//            twice), then the maximum, the sum and P = 2^(S log2 e - max) /
+//            sum in fp16, with zeros from the last visible key up to the end
+//            of the last tile the P.V kernel reads for that row, and the
+//            row's log-sum-exp.  Loads and stores go through buffer views
+//            that end at the row's last visible chunk and at the end of its
+//            padding, so no lane needs a bounds branch.
 //   pv       O = P V.  A = 16 keys of P per lane, read straight from HBM;
 //            B = V from a row-major fp16 copy of the 64-key tile in LDS, read
 //            with the transposing LDS load (four keys of one column per
 //            read); fp32 accumulation, one rounding to the output type.
-// The score matrix costs 4 bytes written and up to 8 read per visible score,
-// and P 2 written and 2 read: the traffic the fused kernel never makes.
+// Per visible score the path writes S (4 bytes) and P (2) and reads each
+// once: the traffic the fused kernel never makes.
 #include "fa_common.h"
 #include "fa_internal.h"
 
@@ -87,6 +90,9 @@ __device__ __forceinline__ void tile_load(const void *base, int b, int g, int Hk
     }
 }
 
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+constexpr int kRsrcFlags = 0x00020000;   // buffer descriptor word 3 for raw 32-bit element access
+
 template <typename TIN, int D, bool CAUSAL>
 __global__ __launch_bounds__(UNT) void unfused_scores_kernel(UnfusedArgs a) {
     using S = typename TIN::scalar;
@@ -108,7 +114,8 @@ __global__ __launch_bounds__(UNT) void unfused_scores_kernel(UnfusedArgs a) {
     const int g = bid % a.Hkv;
     bid /= a.Hkv;
     const int b = bid % a.B;
-    const int mb = bid / a.B;
+    const int mbi = bid / a.B;
+    const int mb = CAUSAL ? a.nmb - 1 - mbi : mbi;   // longest rows first
     const Slot sl = slot_of(a, w, mb, hg, g);
     const int Nq = a.Nq, Nk = a.Nk, off = Nk - Nq;
 
@@ -118,6 +125,8 @@ __global__ __launch_bounds__(UNT) void unfused_scores_kernel(UnfusedArgs a) {
     if (t0 >= t1) return;   // the same for the whole workgroup
     const bool live = sl.row0 < Nq;
     const int kend_w = live ? kend_row(min(sl.row0 + UR, Nq) - 1, Nq, Nk, CAUSAL) : 0;
+    // keys every row of the slot sees: tiles below need no mask
+    const int kfree_w = live ? kend_row(sl.row0, Nq, Nk, CAUSAL) : 0;
 
     V8 qf[KSTEPS];
     {
@@ -126,7 +135,15 @@ __global__ __launch_bounds__(UNT) void unfused_scores_kernel(UnfusedArgs a) {
 #pragma unroll
         for (int ks = 0; ks < KSTEPS; ++ks) qf[ks] = as_vec8<V8>(ld16(qp + 16 * ks));
     }
-    float *srow = a.s + ((size_t)((size_t)b * a.Hq + sl.h) * Nq) * a.NkP;
+    // The slot's 32 rows of S as a buffer view ending after row Nq - 1: stores
+    // to rows past the end fall outside it and are dropped.  Lane l stores key
+    // (l % 32) of rows 8 (r / 4) + 4 (l / 32) + r % 4 (byte offsets stay below
+    // 2^31: Nk <= 2^23).
+    const int nrows = live ? min(UR, Nq - sl.row0) : 0;
+    const __amdgpu_buffer_rsrc_t srs = __builtin_amdgcn_make_buffer_rsrc(
+        a.s + ((size_t)((size_t)b * a.Hq + sl.h) * Nq + (live ? sl.row0 : 0)) * a.NkP, (short)0,
+        nrows * a.NkP * 4, kRsrcFlags);
+    const int lane_off = (4 * lh * a.NkP + lq) * 4;
 
     uint4_t kr[NLD];
     tile_load<TIN, D>(a.k, b, g, a.Hkv, Nk, t0 * UKT, tid, kr);
@@ -140,37 +157,32 @@ __global__ __launch_bounds__(UNT) void unfused_scores_kernel(UnfusedArgs a) {
         __syncthreads();
         if (t + 1 < t1) tile_load<TIN, D>(a.k, b, g, a.Hkv, Nk, (t + 1) * UKT, tid, kr);
         if (t * UKT >= kend_w) continue;   // wave-uniform: no row of the slot sees this tile
+        const bool masked = t * UKT + UKT > kfree_w;   // wave-uniform
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
             float16_t s = float16_t{};
 #pragma unroll
             for (int ks = 0; ks < KSTEPS; ++ks)
                 s = mfma32(qf[ks], as_vec8<V8>(*reinterpret_cast<const uint4_t *>(kt + (32 * half + lq) * KS + 8 * lh + 16 * ks)), s);
-            // lane l holds key (l % 32) of rows 8 (r / 4) + 4 (l / 32) + r % 4
-            const int key = t * UKT + 32 * half + lq;
+            const int k0 = t * UKT + 32 * half;
+            const int voff = lane_off + k0 * 4;
+            // causal: key visible to row (row0 + 4 lh + dr) iff key - off - row0 - 4 lh <= dr
+            const int kd = k0 + lq - off - sl.row0 - 4 * lh;
+            const bool kin = k0 + lq < Nk;
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                const int row = sl.row0 + 8 * (r >> 2) + 4 * lh + (r & 3);
-                if (row < Nq) {
-                    const bool vis = key < Nk && (!CAUSAL || key <= row + off);
-                    srow[(size_t)row * a.NkP + key] = vis ? s[r] * a.scale : -INFINITY;
-                }
+                const int dr = 8 * (r >> 2) + (r & 3);
+                float val = s[r] * a.scale;
+                if (masked) val = (kin && (!CAUSAL || kd <= dr)) ? val : -INFINITY;
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(val), srs, voff + dr * a.NkP * 4, 0, 0);
             }
         }
     }
 }
 
-// Maximum and sum pair of two lanes' partial states (log2 domain).
-__device__ __forceinline__ void lse_combine(float &m, float &sum, float m2, float s2) {
-    const float M = __builtin_fmaxf(m, m2);
-    const float a = (m == -INFINITY) ? 0.f : sum * exp2_fast(m - M);
-    const float b = (m2 == -INFINITY) ? 0.f : s2 * exp2_fast(m2 - M);
-    m = M;
-    sum = a + b;
-}
-
 template <bool CAUSAL>
 __global__ __launch_bounds__(UNT) void unfused_softmax_kernel(UnfusedArgs a) {
+    constexpr int CH = 16;   // 16-byte chunks per lane held in registers: the first 4096 keys
     const int tid = threadIdx.x, l = tid & 63;
     const long long row = (long long)blockIdx.x * USLOT + (tid >> 6);
     if (row >= (long long)a.B * a.Hq * a.Nq) return;   // no barrier below
@@ -179,42 +191,91 @@ __global__ __launch_bounds__(UNT) void unfused_softmax_kernel(UnfusedArgs a) {
     // the P.V kernel reads whole 64-key tiles up to the extent of the last
     // row of this row's 32-row slot, at most 31 keys past this row's own
     const int zend = min(a.NkP, ((kend + UKT - 1) / UKT) * UKT + UKT);
-    const float *sr = a.s + (size_t)row * a.NkP;
+    float *sr = a.s + (size_t)row * a.NkP;
     _Float16 *pr = a.p + (size_t)row * a.NkP;
+    const int kc = min(kend, CH * 256);
+    // views of the row: S up to the last visible chunk (loads past it return
+    // zero and read no memory), P up to the end of the zero padding
+    const __amdgpu_buffer_rsrc_t srs = __builtin_amdgcn_make_buffer_rsrc(sr, (short)0, ((kc + 3) & ~3) * 4, kRsrcFlags);
+    const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(pr, (short)0, zend * 2, kRsrcFlags);
 
-    float m = -INFINITY, sum = 0.f;
-    for (int c = 4 * l; c < kend; c += 256) {
-        const float4_t x = *reinterpret_cast<const float4_t *>(sr + c);
+    const int nch = (kc + 255) / 256;   // held chunks with visible keys (wave-uniform)
+    float4_t x[CH];
+#pragma unroll
+    for (int j = 0; j < CH; ++j) {
+        x[j] = float4_t{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+        if (j < nch)
+            x[j] = __builtin_bit_cast(float4_t, __builtin_amdgcn_raw_buffer_load_b128(srs, (4 * l + 256 * j) * 4, 0, 0));
+    }
+    float m = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < CH; ++j) {
+        if (j < nch) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float t = (4 * l + 256 * j + e < kend) ? x[j][e] * kLog2e : -INFINITY;
+                x[j][e] = t;
+                m = __builtin_fmaxf(m, t);
+            }
+        }
+    }
+    // keys past the held part (rows longer than 4096 keys): running maximum
+    // and sum, read again for the weights
+    float mt = -INFINITY, st = 0.f;
+    for (int c = CH * 256 + 4 * l; c < kend; c += 256) {
+        const float4_t y = *reinterpret_cast<const float4_t *>(sr + c);
         float t[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) t[e] = (c + e < kend) ? x[e] * kLog2e : -INFINITY;
+        for (int e = 0; e < 4; ++e) t[e] = (c + e < kend) ? y[e] * kLog2e : -INFINITY;
         const float mx = __builtin_fmaxf(__builtin_fmaxf(t[0], t[1]), __builtin_fmaxf(t[2], t[3]));
-        if (mx > m) {
-            sum = (m == -INFINITY) ? 0.f : sum * exp2_fast(m - mx);
-            m = mx;
+        if (mx > mt) {
+            st = (mt == -INFINITY) ? 0.f : st * exp2_fast(mt - mx);
+            mt = mx;
         }
 #pragma unroll
-        for (int e = 0; e < 4; ++e) sum += exp2_fast(t[e] - m);
+        for (int e = 0; e < 4; ++e) st += exp2_fast(t[e] - mt);
+    }
+    float M = __builtin_fmaxf(m, mt);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) M = __builtin_fmaxf(M, __shfl_xor(M, o));
+    float sum = (mt == -INFINITY) ? 0.f : st * exp2_fast(mt - M);
+#pragma unroll
+    for (int j = 0; j < CH; ++j) {
+        if (j < nch) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) sum += exp2_fast(x[j][e] - M);
+        }
     }
 #pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-        const float m2 = __shfl_xor(m, o), s2 = __shfl_xor(sum, o);
-        lse_combine(m, sum, m2, s2);
-    }
+    for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o);
     const float inv = 1.f / sum;
-    if (a.lse && l == 0) a.lse[row] = (m + __builtin_log2f(sum)) * kLn2;
-    for (int c = 4 * l; c < zend; c += 256) {
-        half4_t out = {(_Float16)0.f, (_Float16)0.f, (_Float16)0.f, (_Float16)0.f};
+    if (a.lse && l == 0) a.lse[row] = (M + __builtin_log2f(sum)) * kLn2;
+#pragma unroll
+    for (int j = 0; j < CH; ++j) {
+        if (256 * j < zend) {
+            half4_t h = {(_Float16)0.f, (_Float16)0.f, (_Float16)0.f, (_Float16)0.f};
+            if (j < nch) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) h[e] = (_Float16)(exp2_fast(x[j][e] - M) * inv);
+            }
+            __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2_t, h), prs, (4 * l + 256 * j) * 2, 0, 0);
+        }
+    }
+    for (int c = CH * 256 + 4 * l; c < zend; c += 256) {
+        half4_t h = {(_Float16)0.f, (_Float16)0.f, (_Float16)0.f, (_Float16)0.f};
         if (c < kend) {
-            const float4_t x = *reinterpret_cast<const float4_t *>(sr + c);
+            const float4_t y = *reinterpret_cast<const float4_t *>(sr + c);
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-                out[e] = (c + e < kend) ? (_Float16)(exp2_fast(x[e] * kLog2e - m) * inv) : (_Float16)0.f;
+                h[e] = (c + e < kend) ? (_Float16)(exp2_fast(y[e] * kLog2e - M) * inv) : (_Float16)0.f;
         }
-        *reinterpret_cast<half4_t *>(pr + c) = out;
+        *reinterpret_cast<half4_t *>(pr + c) = h;
     }
 }
 
+// P.V: the workgroup's four slots share each staged V tile (the slot layout
+// of the scores kernel, longest rows first).  Each tile's P loads are issued
+// before the workgroup stages the V tile, so the two overlap.
 template <typename TIN, typename TOUT, int D, bool CAUSAL>
 __global__ __launch_bounds__(UNT) void unfused_pv_kernel(UnfusedArgs a) {
     constexpr int VS = D + 8;            // LDS row stride (fp16 elements)
@@ -233,7 +294,7 @@ __global__ __launch_bounds__(UNT) void unfused_pv_kernel(UnfusedArgs a) {
     const int g = bid % a.Hkv;
     bid /= a.Hkv;
     const int b = bid % a.B;
-    const int mb = bid / a.B;
+    const int mb = CAUSAL ? a.nmb - 1 - bid / a.B : bid / a.B;   // longest rows first
     const Slot sl = slot_of(a, w, mb, hg, g);
     const int Nq = a.Nq, Nk = a.Nk;
 
@@ -298,17 +359,17 @@ __global__ __launch_bounds__(UNT) void unfused_pv_kernel(UnfusedArgs a) {
 
 template <typename TIN, typename TOUT, int D, bool CAUSAL>
 hipError_t launch_t(const UnfusedArgs &a, hipStream_t s) {
-    const long long per = (long long)a.nmb * a.B * a.Hkv * a.nhg;
-    const long long nsc = per * a.nchunk;
+    const long long nsc = (long long)a.nmb * a.B * a.Hkv * a.nhg * a.nchunk;
     const long long nrow = ((long long)a.B * a.Hq * a.Nq + USLOT - 1) / USLOT;
-    if (nsc > 0x7fffffffLL || nrow > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+    const long long npv = (long long)a.nmb * a.B * a.Hkv * a.nhg;
+    if (nsc > 0x7fffffffLL || nrow > 0x7fffffffLL || npv > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL((unfused_scores_kernel<TIN, D, CAUSAL>), dim3((unsigned)nsc), dim3(UNT), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((unfused_softmax_kernel<CAUSAL>), dim3((unsigned)nrow), dim3(UNT), 0, s, a);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((unfused_pv_kernel<TIN, TOUT, D, CAUSAL>), dim3((unsigned)per), dim3(UNT), 0, s, a);
+    hipLaunchKernelGGL((unfused_pv_kernel<TIN, TOUT, D, CAUSAL>), dim3((unsigned)npv), dim3(UNT), 0, s, a);
     return hipGetLastError();
 }
 

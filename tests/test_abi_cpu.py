@@ -220,3 +220,4 @@ def test_unfused_argument_errors_before_any_launch():
     assert call(ws=Q) == 8                                 # workspace over q
     assert call(ws=O - 256) == 8                           # workspace runs into o
     assert call(o=Q + 64) == 8                             # the checks of fa_fwd come first
+    assert call(B=1, Hq=2, Hkv=1, Nq=1, Nk=(1 << 23) + 1) == 2   # 32-bit offsets in a block of scores

@@ -1,5 +1,6 @@
 """HIP graph capture of the library's calls: prefill, split-KV decode (with
-its merge kernel and workspace), decode against a paged cache and the Q8_0
+its merge kernel and workspace), decode against a paged cache, the unfused
+path (three kernels through a caller workspace) and the Q8_0
 matrix-vector product are captured once after a warm-up call and replayed
 several times, with eager work and synchronisations between the replays;
 every replay must equal the eager result bit for bit.  (The library issues no
@@ -39,12 +40,15 @@ def test_graph_replays_equal_eager():
     sl = torch.tensor([Nk, 1000, 64, 1], dtype=torch.int32, device="cuda")
     # Q8_0 product
     w8, x8 = (t.cuda() for t in make_q8_0(3000, 2048, seed=3, x_dtype="bf16"))
+    # unfused path on the prefill inputs
+    wsu = torch.empty(fa.unfused_workspace_bytes(1, 16, 300, 300), dtype=torch.uint8, device="cuda")
 
     outs = {
         "prefill": (torch.empty_like(qp), torch.empty((1, 16, 300), dtype=torch.float32, device="cuda")),
         "decode": (torch.empty_like(qd), torch.empty((4, 32, 1), dtype=torch.float32, device="cuda")),
         "paged": (torch.empty_like(qd), torch.empty((4, 32, 1), dtype=torch.float32, device="cuda")),
         "q8": (torch.empty(3000, dtype=torch.bfloat16, device="cuda"),),
+        "unfused": (torch.empty_like(qp), torch.empty((1, 16, 300), dtype=torch.float32, device="cuda")),
     }
 
     def calls():
@@ -52,6 +56,8 @@ def test_graph_replays_equal_eager():
         fa.fwd(qd, kd, vd, out=outs["decode"][0], lse=outs["decode"][1])
         fa.fwd_kvcache_paged(qd, kpg, vpg, table, sl, out=outs["paged"][0], lse=outs["paged"][1])
         fa.q8_0_gemv(w8, x8, out=outs["q8"][0])
+        fa.fwd_unfused(qp, kp, vp, causal=True, out=outs["unfused"][0], lse=outs["unfused"][1],
+                       workspace=wsu)
 
     calls()
     torch.cuda.synchronize()

@@ -1,6 +1,6 @@
 """Seeded random sweeps of the GPU paths against the fp64 oracles, beside the
 hand-picked cases: shapes, dtypes, masks, scales, head ratios, cache lengths,
-page sizes and Q8_0 matrix sizes drawn from fixed seeds (the draw is printed
+page sizes, Q8_0 matrix sizes and unfused-path shapes drawn from fixed seeds (the draw is printed
 with each case so that a failure names it).
 
 Attention: every output and lse compared in verify mode (fp32 output of the
@@ -125,3 +125,32 @@ def test_random_q8_gemv_against_oracle(seed):
         bound = bound + 2.0 ** -11 * (np.abs(ref) + bound) + 2.0 ** -25
     err = np.abs(y.float().cpu().numpy().astype(np.float64) - ref)
     assert np.all(err <= bound), label
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_unfused_against_oracle(seed):
+    """The unfused path (fa_fwd_unfused) on drawn shapes, every output and lse
+    against the oracle in verify mode and as shipped."""
+    r = random.Random(1200 + seed)
+    dt = r.choice(["bf16", "f16"])
+    D = r.choice([64, 128])
+    Hkv = r.choice([1, 2, 4])
+    Hq = Hkv * r.choice([1, 2, 3, 4, 8])
+    B = r.choice([1, 2])
+    Nk = r.randint(1, 600)
+    causal = r.random() < 0.6
+    Nq = r.randint(1, Nk) if causal else r.randint(1, 600)
+    scale = r.choice([None, 0.5, -0.3])
+    if scale is None:
+        scale = 1.0 / np.sqrt(D)
+    label = f"seed {seed}: unfused B{B} Hq{Hq} Hkv{Hkv} Nq{Nq} Nk{Nk} D{D} causal={causal} {dt} scale={scale}"
+    print(label, flush=True)
+    q, k, v = make_qkv(B, Hq, Hkv, Nq, Nk, D, dt, seed=40_000 + seed)
+    o_ref, l_ref = oracle_full(q, k, v, causal, scale)
+    qd, kd, vd = q.cuda(), k.cuda(), v.cuda()
+    o, lse = fa.fwd_unfused(qd, kd, vd, causal=causal, scale=scale, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    check_against(o, lse, o_ref, l_ref, DTYPES[dt], True, label)
+    o2, lse2 = fa.fwd_unfused(qd, kd, vd, causal=causal, scale=scale)
+    torch.cuda.synchronize()
+    check_against(o2, lse2, o_ref, l_ref, DTYPES[dt], False, label + " shipped")
