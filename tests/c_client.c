@@ -1,15 +1,17 @@
 /*
  * c_client.c -- a plain C caller of the library (no PyTorch): reads a problem
- * and its inputs from a file, copies them to device memory, calls fa_fwd (and
- * fa_q8_0_gemv) through the C ABI on the null stream, and writes the outputs
- * to a file.  Used by tests/test_c_client_gpu.py; built by __graft_entry__.build().
+ * and its inputs from a file, copies them to device memory, calls fa_fwd,
+ * fa_q8_0_gemv and (fp16 / bf16 inputs) fa_fwd_unfused with a workspace of
+ * its own through the C ABI on the null stream, and writes the outputs to a
+ * file.  Used by tests/test_c_client_gpu.py; built by __graft_entry__.build().
  *
  * Input file (little-endian):
  *   int32  B, Hq, Hkv, Nq, Nk, D, causal, in_dtype   then float32 scale
  *   q, k, v as raw elements of in_dtype
  *   int32  M, K   then M * K / 32 * 34 bytes of Q8_0 weights and K float32 x
  * Output file:
- *   o (float32, B*Nq*Hq*D), lse (float32, B*Hq*Nq), y (float32, M)
+ *   o (float32, B*Nq*Hq*D), lse (float32, B*Hq*Nq), y (float32, M), then for
+ *   fp16 / bf16 inputs the unfused path's o and lse (float32, same shapes)
  * Exit status 0 on success; otherwise the failing call is printed.
  */
 #include <hip/hip_runtime_api.h>
@@ -90,6 +92,31 @@ int main(int argc, char **argv) {
         fprintf(stderr, "fa_q8_0_gemv: %s\n", fa_status_string(st));
         return 3;
     }
+    /* the unfused path into a second pair of outputs, workspace from hipMalloc */
+    float *dout2 = NULL, *dlse2 = NULL;
+    void *dws = NULL;
+    const int unfused = dt != FA_F32;
+    if (unfused) {
+        const size_t wsb = fa_unfused_workspace_bytes(B, Hq, Nq, Nk);
+        if (wsb == 0) {
+            fprintf(stderr, "fa_unfused_workspace_bytes returned 0\n");
+            return 3;
+        }
+        HIP_OK(hipMalloc((void **)&dout2, nq * 4));
+        HIP_OK(hipMalloc((void **)&dlse2, nl * 4));
+        HIP_OK(hipMalloc(&dws, wsb));
+        if (fa_fwd_unfused(dq, dk, dv, dout2, dlse2, B, Hq, Hkv, Nq, Nk, D, causal, scale, NULL, dt,
+                           FA_F32, dws, wsb - 1) != FA_ERR_WORKSPACE) {
+            fprintf(stderr, "a short workspace was accepted\n");
+            return 3;
+        }
+        st = fa_fwd_unfused(dq, dk, dv, dout2, dlse2, B, Hq, Hkv, Nq, Nk, D, causal, scale, NULL, dt,
+                            FA_F32, dws, wsb);
+        if (st != FA_OK) {
+            fprintf(stderr, "fa_fwd_unfused: %s\n", fa_status_string(st));
+            return 3;
+        }
+    }
     HIP_OK(hipDeviceSynchronize());
 
     float *ho = (float *)malloc(nq * 4), *hl = (float *)malloc(nl * 4), *hy = (float *)malloc((size_t)M * 4);
@@ -101,8 +128,13 @@ int main(int argc, char **argv) {
     if (!out || fwrite(ho, 4, nq, out) != nq || fwrite(hl, 4, nl, out) != nl ||
         fwrite(hy, 4, (size_t)M, out) != (size_t)M)
         return 1;
+    if (unfused) {
+        HIP_OK(hipMemcpy(ho, dout2, nq * 4, hipMemcpyDeviceToHost));
+        HIP_OK(hipMemcpy(hl, dlse2, nl * 4, hipMemcpyDeviceToHost));
+        if (fwrite(ho, 4, nq, out) != nq || fwrite(hl, 4, nl, out) != nl) return 1;
+    }
     fclose(out);
     fa_release_workspace();
-    printf("c_client: fa_fwd and fa_q8_0_gemv done\n");
+    printf("c_client: fa_fwd, fa_q8_0_gemv%s done\n", unfused ? " and fa_fwd_unfused" : "");
     return 0;
 }

@@ -1,8 +1,9 @@
 """The C ABI used from plain C, without PyTorch: tests/c_client (built by
-__graft_entry__.build()) reads inputs from a file, calls fa_fwd and
-fa_q8_0_gemv on device buffers it allocates itself, and writes the results;
-they are compared with the fp64 oracles (attention in verify mode within
-2e-3, the Q8_0 product within its derived fp32 bound)."""
+__graft_entry__.build()) reads inputs from a file, calls fa_fwd,
+fa_q8_0_gemv and (fp16 / bf16) fa_fwd_unfused on device buffers and a
+workspace it allocates itself, and writes the results; they are compared
+with the fp64 oracles (attention in verify mode within 2e-3, the Q8_0
+product within its derived fp32 bound)."""
 import os
 import struct
 import subprocess
@@ -56,7 +57,7 @@ def test_c_client_matches_oracle(case, tmp_path):
     no, nl = B * Nq * Hq * D, B * Hq * Nq
     o = torch.from_numpy(data[:no].reshape(B, Nq, Hq, D).copy())
     lse = torch.from_numpy(data[no:no + nl].reshape(B, Hq, Nq).copy())
-    y = data[no + nl:].astype(np.float64)
+    y = data[no + nl:no + nl + M].astype(np.float64)
     o_ref, l_ref = oracle.attention(q, k, v, bool(causal), scale)
     check_against(o, lse, o_ref, l_ref, DTYPES[dt], True, f"c_client {case}")
     ref = oracle_q8.gemv(w.numpy(), x.numpy())
@@ -66,3 +67,11 @@ def test_c_client_matches_oracle(case, tmp_path):
     qa = np.abs(np.ascontiguousarray(wn[:, :, 2:]).view(np.int8).astype(np.float64))
     S = (d * (qa * np.abs(x.numpy().astype(np.float64)).reshape(1, nb, 32)).sum(axis=2)).sum(axis=1)
     assert np.all(np.abs(y - ref) <= (2 * nb + 64) * 2.0 ** -24 * S)
+    rest = data[no + nl + M:]
+    if dt == "f32":
+        assert rest.size == 0
+    else:
+        assert rest.size == no + nl
+        o2 = torch.from_numpy(rest[:no].reshape(B, Nq, Hq, D).copy())
+        l2 = torch.from_numpy(rest[no:].reshape(B, Hq, Nq).copy())
+        check_against(o2, l2, o_ref, l_ref, DTYPES[dt], True, f"c_client unfused {case}")
