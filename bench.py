@@ -237,6 +237,47 @@ def paged_decode(torch, fa, w, steps, warmup, page_size):
     return ms * 1e3, w.kv_bytes() / (ms * 1e-3) / 1e9
 
 
+def chunked_prefill(torch, fa, steps, warmup):
+    """Chunked prefill: 512 new query tokens per sequence against K/V caches
+    whose valid lengths are 4096, 3072, 2048 and 1024 (the headline model's
+    heads: 32 query / 8 key-value heads, D = 64, bf16, causal, bottom-right
+    per sequence), on the contiguous cache and on the same cache in shuffled
+    pages of 256 keys.  FLOPs: 4 D per visible (query, key) pair per head."""
+    from paper_2608_18656_amd.inputs import make_qkv
+
+    B, Hq, Hkv, Nq, Nk, D, ps = 4, 32, 8, 512, 4096, 64, 256
+    lens = [4096, 3072, 2048, 1024]
+    q, k, v = make_qkv(B, Hq, Hkv, Nq, Nk, D, "bf16", seed=5000)
+    vis = sum(Nq * (L - Nq + 1) + Nq * (Nq - 1) // 2 for L in lens)
+    flops = 4 * D * Hq * vis
+    qd, kd, vd = q.cuda(), k.cuda(), v.cuda()
+    sl = torch.tensor(lens, dtype=torch.int32, device="cuda")
+    out = torch.empty_like(qd)
+    lse = torch.empty((B, Hq, Nq), dtype=torch.float32, device="cuda")
+    scale = D ** -0.5
+    ms_c = time_calls(torch, [lambda: fa.fwd_kvcache(qd, kd, vd, sl, causal=True, scale=scale, out=out,
+                                                     lse=lse)], steps, warmup)
+    npg = B * (Nk // ps)
+    perm = torch.randperm(npg, generator=torch.Generator().manual_seed(5001))
+    kp = torch.empty((npg, ps, Hkv, D), dtype=k.dtype)
+    vp = torch.empty_like(kp)
+    kp[perm] = k.reshape(npg, ps, Hkv, D)
+    vp[perm] = v.reshape(npg, ps, Hkv, D)
+    table = perm.reshape(B, -1).to(torch.int32).cuda()
+    kp, vp = kp.cuda(), vp.cuda()
+    ms_p = time_calls(torch, [lambda: fa.fwd_kvcache_paged(qd, kp, vp, table, sl, causal=True, scale=scale,
+                                                           out=out, lse=lse)], steps, warmup)
+    res = {"metric": "chunked prefill TFLOP/s (4 D FLOPs per visible pair per head)",
+           "shape": {"B": B, "Hq": Hq, "Hkv": Hkv, "Nq": Nq, "Nk": Nk, "D": D, "seqlens": lens,
+                     "dtype": "bf16", "causal": True},
+           "flops": flops}
+    for label, ms in (("contiguous", ms_c), ("paged256", ms_p)):
+        tf = flops / (ms * 1e-3) / 1e12
+        res[label] = {"us_per_call": round(ms * 1e3, 2), "tflops": round(tf, 1),
+                      "frac": round(tf / PEAK_MFMA_TFLOPS["bf16"], 4)}
+    return res
+
+
 def q8_decode_step(torch, fa, steps, warmup, with_cpu):
     """The Q8_0 matrix-vector products of one decode step of a TinyLlama-1.1B
     shaped model (22 layers; per layer the fused q/k/v projection, the output
@@ -500,6 +541,10 @@ def main():
                                                              f"{xw.name}_paged{ps}", DECODE_SOURCES)})
             log(f"[bench] paged decode, pages of {ps}: {pus:.1f} us/call, {pgbs:.0f} GB/s")
         result["paged_decode"] = paged
+        cp = chunked_prefill(torch, fa, max(5, min(args.steps, 30)), 3)
+        result["chunked_prefill"] = cp
+        log(f"[bench] chunked prefill 4 x 512 new tokens: {cp['contiguous']['us_per_call']} us "
+            f"({cp['contiguous']['tflops']} TFLOP/s), paged 256: {cp['paged256']['us_per_call']} us")
         result["q8_0_gemv"] = q8_decode_step(torch, fa, max(5, min(args.steps, 20)), 3,
                                              not args.no_cpu_baseline)
         # achievable HBM bandwidth for context: a plain 1 GiB device copy

@@ -193,16 +193,31 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
     const S *tnext = kvbase;
     long long rem = (long long)(Nk - 1) * (long long)row_elems * (long long)sizeof(S) +
                     (long long)D * (long long)sizeof(S);
-    // paged K/V: the pool of pages, at head g
+    // paged K/V: the pool of pages, at head g.  Tiles are loaded in order
+    // and a page holds a whole number of tiles, so the page index and the
+    // offset inside the page advance without a division.  The table entry of
+    // the following page is read ahead with a vector load through a view of
+    // this sequence's row of the table (entries past the row read as zero),
+    // so it has arrived when the page is reached, and no scalar load (whose
+    // counter the LDS reads share) is in flight during a step.
     const S *kvpool = reinterpret_cast<const S *>(kgroup ? a.k : a.v) + (size_t)g * D;
+    const __amdgpu_buffer_rsrc_t trs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<int *>(PAGED ? a.block_table + (size_t)b * a.max_pages : nullptr), (short)0,
+        PAGED ? a.max_pages * 4 : 0, 0x00020000);
+    const size_t page_elems = (size_t)a.page_size * row_elems;
+    int pidx = 0, poff = 0;   // page index and key offset of the next tile
+    int tcur = 0, tnx = 0;    // table entries of pages pidx and pidx + 1
+    if constexpr (PAGED) {
+        tcur = __builtin_amdgcn_raw_buffer_load_b32(trs, 0, 0, 0);
+        tnx = __builtin_amdgcn_raw_buffer_load_b32(trs, 4, 0, 0);
+    }
     auto gload = [&](int kt) {   // the next tile (tiles are loaded in order; the argument is its first key)
         if constexpr (PAGED) {
             // the tile's rows sit in one page (pages hold a multiple of 64
             // keys, tiles start at multiples of BC); the view ends after the
             // last valid key of the tile; page numbers are clamped into the pool
-            const int pi = kt / a.page_size;
-            const int page = min(max(a.block_table[(size_t)b * a.max_pages + pi], 0), a.num_pages - 1);
-            tnext = kvpool + ((size_t)page * a.page_size + (kt - pi * a.page_size)) * row_elems;
+            const int page = min(max(__builtin_amdgcn_readfirstlane(tcur), 0), a.num_pages - 1);
+            tnext = kvpool + (size_t)page * page_elems + (size_t)poff * row_elems;
             rem = (long long)(min(Nk - kt, BC) - 1) * (long long)row_elems * (long long)sizeof(S) +
                   (long long)D * (long long)sizeof(S);
         }
@@ -220,6 +235,13 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
         if constexpr (!PAGED) {
             tnext += (size_t)BC * row_elems;
             rem -= (long long)BC * (long long)row_elems * (long long)sizeof(S);
+        } else {
+            poff += BC;
+            const bool cross = poff == a.page_size;   // wave-uniform
+            tcur = cross ? tnx : tcur;
+            poff = cross ? 0 : poff;
+            pidx += cross ? 1 : 0;
+            tnx = __builtin_amdgcn_raw_buffer_load_b32(trs, (pidx + 1) * 4, 0, 0);
         }
     };
     // LDS destination (element offset inside a stage) of load i
