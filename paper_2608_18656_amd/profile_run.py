@@ -17,6 +17,13 @@ of that size in a seeded random order.
 softmax and P.V kernels through a workspace) on a prefill workload.
 
     python3 paper_2608_18656_amd/profile_run.py unfused_gqa_prefill_bf16 5
+
+``chunked_prefill`` runs the chunked prefill of the benchmark (512 new
+tokens per sequence against caches of 4096, 3072, 2048 and 1024 keys, 32/8
+heads, D = 64, bf16, causal) on the contiguous cache, then on the same cache
+in shuffled pages of 256 keys.
+
+    python3 paper_2608_18656_amd/profile_run.py chunked_prefill 20
 """
 from __future__ import annotations
 
@@ -71,6 +78,28 @@ def main(argv):
             fa.q8_0_gemv(w, x)
         torch.cuda.synchronize()
         print(f"ran {what} {shape} x {reps}", flush=True)
+        return
+    if what == "chunked_prefill":
+        from paper_2608_18656_amd.inputs import make_qkv
+
+        B, Hq, Hkv, Nq, Nk, D, ps = 4, 32, 8, 512, 4096, 64, 256
+        q, k, v = make_qkv(B, Hq, Hkv, Nq, Nk, D, "bf16", seed=5000)
+        sl = torch.tensor([4096, 3072, 2048, 1024], dtype=torch.int32, device="cuda")
+        npg = B * (Nk // ps)
+        perm = torch.randperm(npg, generator=torch.Generator().manual_seed(5001))
+        kp = torch.empty((npg, ps, Hkv, D), dtype=k.dtype)
+        vp = torch.empty_like(kp)
+        kp[perm] = k.reshape(npg, ps, Hkv, D)
+        vp[perm] = v.reshape(npg, ps, Hkv, D)
+        table = perm.reshape(B, -1).to(torch.int32).cuda()
+        qd, kd, vd, kp, vp = q.cuda(), k.cuda(), v.cuda(), kp.cuda(), vp.cuda()
+        for _ in range(reps):
+            fa.fwd_kvcache(qd, kd, vd, sl, causal=True, scale=D ** -0.5)
+        torch.cuda.synchronize()
+        for _ in range(reps):
+            fa.fwd_kvcache_paged(qd, kp, vp, table, sl, causal=True, scale=D ** -0.5)
+        torch.cuda.synchronize()
+        print(f"ran {what} x {reps} (contiguous, then paged)", flush=True)
         return
     if what.startswith("unfused_"):
         w = WORKLOADS[what[len("unfused_"):]]
