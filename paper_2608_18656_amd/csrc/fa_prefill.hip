@@ -205,6 +205,8 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
         const_cast<int *>(PAGED ? a.block_table + (size_t)b * a.max_pages : nullptr), (short)0,
         PAGED ? a.max_pages * 4 : 0, 0x00020000);
     const size_t page_elems = (size_t)a.page_size * row_elems;
+    const int row_bytes = (int)(row_elems * sizeof(S));                 // paged: one key row of the pool
+    const int tile_bytes = (BC - 1) * row_bytes + D * (int)sizeof(S);    // paged: view of a full tile
     int pidx = 0, poff = 0;   // page index and key offset of the next tile
     int tcur = 0, tnx = 0;    // table entries of pages pidx and pidx + 1
     if constexpr (PAGED) {
@@ -212,21 +214,28 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
         tnx = __builtin_amdgcn_raw_buffer_load_b32(trs, 4, 0, 0);
     }
     auto gload = [&](int kt) {   // the next tile (tiles are loaded in order; the argument is its first key)
+        int nrec;
         if constexpr (PAGED) {
             // the tile's rows sit in one page (pages hold a multiple of 64
-            // keys, tiles start at multiples of BC); the view ends after the
-            // last valid key of the tile; page numbers are clamped into the pool
-            const int page = min(max(__builtin_amdgcn_readfirstlane(tcur), 0), a.num_pages - 1);
-            tnext = kvpool + (size_t)page * page_elems + (size_t)poff * row_elems;
-            rem = (long long)(min(Nk - kt, BC) - 1) * (long long)row_elems * (long long)sizeof(S) +
-                  (long long)D * (long long)sizeof(S);
+            // keys, tiles start at multiples of BC): at the start of a page
+            // the base comes from the table (page numbers clamped into the
+            // pool), within it the base advances by one tile per load; the
+            // view ends after the last valid key of the tile (one tile's
+            // extent, which fits 31 bits)
+            if (poff == 0) {
+                const int page = min(max(__builtin_amdgcn_readfirstlane(tcur), 0), a.num_pages - 1);
+                tnext = kvpool + (size_t)page * page_elems;
+            }
+            const int left = Nk - kt;
+            nrec = left >= BC ? tile_bytes : (left - 1) * row_bytes + D * (int)sizeof(S);
+        } else {
+            // view range, clamped to 31 bits (the tile's own extent always
+            // fits); the halves are opaque so that the test stays two 32-bit
+            // scalar compares instead of one 64-bit vector compare
+            unsigned rlo = (unsigned)rem, rhi = (unsigned)(rem >> 32);
+            asm volatile("" : "+s"(rlo), "+s"(rhi));
+            nrec = (int)(rhi != 0u ? 0x7fffffffu : __builtin_elementwise_min(rlo, 0x7fffffffu));
         }
-        // view range, clamped to 31 bits (the tile's own extent always fits);
-        // the halves are opaque so that the test stays two 32-bit scalar
-        // compares instead of one 64-bit vector compare
-        unsigned rlo = (unsigned)rem, rhi = (unsigned)(rem >> 32);
-        asm volatile("" : "+s"(rlo), "+s"(rhi));
-        const int nrec = (int)(rhi != 0u ? 0x7fffffffu : __builtin_elementwise_min(rlo, 0x7fffffffu));
         const __amdgpu_buffer_rsrc_t rs =
             __builtin_amdgcn_make_buffer_rsrc(const_cast<S *>(tnext), (short)0, nrec, 0x00020000);
 #pragma unroll
@@ -236,6 +245,7 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
             tnext += (size_t)BC * row_elems;
             rem -= (long long)BC * (long long)row_elems * (long long)sizeof(S);
         } else {
+            tnext += (size_t)BC * row_elems;
             poff += BC;
             const bool cross = poff == a.page_size;   // wave-uniform
             tcur = cross ? tnx : tcur;
