@@ -4,7 +4,8 @@ same seeded input bits, element by element.  Tolerance rules in helpers.py.
 Coverage: the six benchmark workloads at sizes the oracle finishes in seconds
 (spanning several tiles and a ragged tail) with every output compared; the
 two decode workloads at full size with every output compared; the three
-prefill workloads at full size on sampled rows; edge shapes (Nk = 1, ragged
+prefill workloads at full size on sampled rows and with every output
+compared (the oracle fanned out over the host's cores); edge shapes (Nk = 1, ragged
 tiles, causal with Nq < Nk, group sizes 1 to 32, odd group sizes, negative
 and zero scale, the vector-ALU path for fp32 and other head dimensions);
 forced split counts including empty splits; determinism; error reporting;
@@ -84,6 +85,26 @@ def test_prefill_full_size_sampled_rows(name):
               f"adjusted {adj:.3e} lse {le:.3e}", flush=True)
     # a property that holds at any size: every output element is finite
     assert torch.isfinite(o.float()).all()
+
+
+@pytest.mark.parametrize("name", ["gqa_prefill_bf16", "gqa_prefill_d128_f16", "mqa_prefill_f16"])
+def test_prefill_full_size_every_element(name):
+    """Every output element and lse of the three prefill workloads at full
+    size (the launch configuration the benchmark times), in verify mode and as
+    shipped, against the fp64 oracle fanned out over the host's cores (at most
+    16 processes; a few seconds per workload on the GPU host)."""
+    w = WORKLOADS[name]
+    q, k, v = make_workload(w)
+    scale = w.softmax_scale
+    print(f"[parity] {name} full size, every element: oracle on {oracle.default_workers()} processes",
+          flush=True)
+    o_ref, l_ref = oracle.attention_parallel(q, k, v, w.causal, scale, workers=oracle.default_workers())
+    for verify in (True, False):
+        o, lse = gpu_attention(q, k, v, w.causal, scale, out_dtype=torch.float32 if verify else None)
+        raw, adj, le = check_against(o, lse, o_ref, l_ref, DTYPES[w.dtype], verify,
+                                     f"{name} full every element verify={verify}")
+        print(f"[parity] {name} full, every element, verify={verify}: raw {raw:.3e} adjusted {adj:.3e} "
+              f"lse {le:.3e}", flush=True)
 
 
 EDGE = [
