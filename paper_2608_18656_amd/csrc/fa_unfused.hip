@@ -12,9 +12,10 @@
 //            64-key tiles; tiles past the causal edge are not computed.
 //            32x32x16 MFMA, A = the wave's 32 query rows (registers),
 //            B = 32 key rows of the tile in LDS.
-//   softmax  one wave per query row: the row's scores are read once into
-//            registers (the first 4096 keys; longer rows stream the rest
-//            twice), then the maximum, the sum and P = 2^(S log2 e - max) /
+//   softmax  one wave per query row, or two or four for rows past 4096
+//            keys: the row's scores are read once into registers (4096 keys
+//            per wave; rows past four waves stream the rest twice), the
+//            waves' maxima and sums combined through LDS, then P = 2^(S log2 e - max) /
 //            sum in fp16, with zeros from the last visible key up to the end
 //            of the last tile the P.V kernel reads for that row, and the
 //            row's log-sum-exp.  Loads and stores go through buffer views
@@ -180,24 +181,32 @@ __global__ __launch_bounds__(UNT) void unfused_scores_kernel(UnfusedArgs a) {
     }
 }
 
-template <bool CAUSAL>
+template <bool CAUSAL, int WPR>
 __global__ __launch_bounds__(UNT) void unfused_softmax_kernel(UnfusedArgs a) {
-    constexpr int CH = 16;   // 16-byte chunks per lane held in registers: the first 4096 keys
-    const int tid = threadIdx.x, l = tid & 63;
-    const long long row = (long long)blockIdx.x * USLOT + (tid >> 6);
-    if (row >= (long long)a.B * a.Hq * a.Nq) return;   // no barrier below
-    const int i = (int)(row % a.Nq);
-    const int kend = kend_row(i, a.Nq, a.Nk, CAUSAL);
+    constexpr int CH = 16;            // 16-byte chunks per lane held in registers
+    constexpr int SEG = CH * 256;     // keys held by one wave (4096)
+    constexpr int RPW = USLOT / WPR;  // rows per workgroup (WPR waves per row)
+    __shared__ float red[USLOT];
+    const int tid = threadIdx.x, l = tid & 63, w = tid >> 6;
+    const int seg = w % WPR;
+    const long long row = (long long)blockIdx.x * RPW + w / WPR;
+    const bool valid = row < (long long)a.B * a.Hq * a.Nq;   // the same for the row's waves
+    // rows past the end take part in the workgroup's barriers and store nothing
+    const long long rr = valid ? row : 0;
+    const int kend = valid ? kend_row((int)(rr % a.Nq), a.Nq, a.Nk, CAUSAL) : 0;
     // the P.V kernel reads whole 64-key tiles up to the extent of the last
     // row of this row's 32-row slot, at most 31 keys past this row's own
-    const int zend = min(a.NkP, ((kend + UKT - 1) / UKT) * UKT + UKT);
-    float *sr = a.s + (size_t)row * a.NkP;
-    _Float16 *pr = a.p + (size_t)row * a.NkP;
-    const int kc = min(kend, CH * 256);
-    // views of the row: S up to the last visible chunk (loads past it return
-    // zero and read no memory), P up to the end of the zero padding
-    const __amdgpu_buffer_rsrc_t srs = __builtin_amdgcn_make_buffer_rsrc(sr, (short)0, ((kc + 3) & ~3) * 4, kRsrcFlags);
-    const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(pr, (short)0, zend * 2, kRsrcFlags);
+    const int zend = valid ? min(a.NkP, ((kend + UKT - 1) / UKT) * UKT + UKT) : 0;
+    float *sr = a.s + (size_t)rr * a.NkP;
+    _Float16 *pr = a.p + (size_t)rr * a.NkP;
+    // this wave's segment of the row: keys k0 .. k0 + SEG - 1, kc of them visible
+    const int k0 = seg * SEG;
+    const int kc = max(0, min(kend - k0, SEG));
+    const int zc = max(0, min(zend - k0, SEG));
+    // views of the segment: S up to its last visible chunk (loads past it
+    // return zero and read no memory), P up to the end of the zero padding
+    const __amdgpu_buffer_rsrc_t srs = __builtin_amdgcn_make_buffer_rsrc(sr + k0, (short)0, ((kc + 3) & ~3) * 4, kRsrcFlags);
+    const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(pr + k0, (short)0, zc * 2, kRsrcFlags);
 
     const int nch = (kc + 255) / 256;   // held chunks with visible keys (wave-uniform)
     float4_t x[CH];
@@ -213,16 +222,17 @@ __global__ __launch_bounds__(UNT) void unfused_softmax_kernel(UnfusedArgs a) {
         if (j < nch) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const float t = (4 * l + 256 * j + e < kend) ? x[j][e] * kLog2e : -INFINITY;
+                const float t = (4 * l + 256 * j + e < kc) ? x[j][e] * kLog2e : -INFINITY;
                 x[j][e] = t;
                 m = __builtin_fmaxf(m, t);
             }
         }
     }
-    // keys past the held part (rows longer than 4096 keys): running maximum
-    // and sum, read again for the weights
+    // keys past the held segments (rows longer than WPR * 4096 keys), in
+    // chunks interleaved over the row's waves: running maximum and sum, read
+    // again for the weights
     float mt = -INFINITY, st = 0.f;
-    for (int c = CH * 256 + 4 * l; c < kend; c += 256) {
+    for (int c = WPR * SEG + 256 * seg + 4 * l; c < kend; c += 256 * WPR) {
         const float4_t y = *reinterpret_cast<const float4_t *>(sr + c);
         float t[4];
 #pragma unroll
@@ -238,6 +248,14 @@ __global__ __launch_bounds__(UNT) void unfused_softmax_kernel(UnfusedArgs a) {
     float M = __builtin_fmaxf(m, mt);
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) M = __builtin_fmaxf(M, __shfl_xor(M, o));
+    const int r0 = w - seg;   // first wave of this row
+    if constexpr (WPR > 1) {
+        if (l == 0) red[w] = M;
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < WPR; ++k) M = __builtin_fmaxf(M, red[r0 + k]);
+        __syncthreads();
+    }
     float sum = (mt == -INFINITY) ? 0.f : st * exp2_fast(mt - M);
 #pragma unroll
     for (int j = 0; j < CH; ++j) {
@@ -248,11 +266,18 @@ __global__ __launch_bounds__(UNT) void unfused_softmax_kernel(UnfusedArgs a) {
     }
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o);
+    if constexpr (WPR > 1) {
+        if (l == 0) red[w] = sum;
+        __syncthreads();
+        sum = 0.f;
+#pragma unroll
+        for (int k = 0; k < WPR; ++k) sum += red[r0 + k];   // fixed order: the same on every wave
+    }
     const float inv = 1.f / sum;
-    if (a.lse && l == 0) a.lse[row] = (M + __builtin_log2f(sum)) * kLn2;
+    if (valid && a.lse && seg == 0 && l == 0) a.lse[row] = (M + __builtin_log2f(sum)) * kLn2;
 #pragma unroll
     for (int j = 0; j < CH; ++j) {
-        if (256 * j < zend) {
+        if (256 * j < zc) {
             half4_t h = {(_Float16)0.f, (_Float16)0.f, (_Float16)0.f, (_Float16)0.f};
             if (j < nch) {
 #pragma unroll
@@ -261,7 +286,7 @@ __global__ __launch_bounds__(UNT) void unfused_softmax_kernel(UnfusedArgs a) {
             __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2_t, h), prs, (4 * l + 256 * j) * 2, 0, 0);
         }
     }
-    for (int c = CH * 256 + 4 * l; c < zend; c += 256) {
+    for (int c = WPR * SEG + 256 * seg + 4 * l; c < zend; c += 256 * WPR) {
         half4_t h = {(_Float16)0.f, (_Float16)0.f, (_Float16)0.f, (_Float16)0.f};
         if (c < kend) {
             const float4_t y = *reinterpret_cast<const float4_t *>(sr + c);
@@ -360,13 +385,20 @@ __global__ __launch_bounds__(UNT) void unfused_pv_kernel(UnfusedArgs a) {
 template <typename TIN, typename TOUT, int D, bool CAUSAL>
 hipError_t launch_t(const UnfusedArgs &a, hipStream_t s) {
     const long long nsc = (long long)a.nmb * a.B * a.Hkv * a.nhg * a.nchunk;
-    const long long nrow = ((long long)a.B * a.Hq * a.Nq + USLOT - 1) / USLOT;
+    const long long nrow = ((long long)a.B * a.Hq * a.Nq + USLOT - 1) / USLOT;   // one wave per row
+    const long long nrow4 = (long long)a.B * a.Hq * a.Nq;                          // four waves per row
     const long long npv = (long long)a.nmb * a.B * a.Hkv * a.nhg;
-    if (nsc > 0x7fffffffLL || nrow > 0x7fffffffLL || npv > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+    if (nsc > 0x7fffffffLL || nrow4 > 0x7fffffffLL || npv > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL((unfused_scores_kernel<TIN, D, CAUSAL>), dim3((unsigned)nsc), dim3(UNT), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((unfused_softmax_kernel<CAUSAL>), dim3((unsigned)nrow), dim3(UNT), 0, s, a);
+    // rows longer than one wave's 4096 held keys take two or four waves
+    if (a.Nk <= 4096)
+        hipLaunchKernelGGL((unfused_softmax_kernel<CAUSAL, 1>), dim3((unsigned)nrow), dim3(UNT), 0, s, a);
+    else if (a.Nk <= 8192)
+        hipLaunchKernelGGL((unfused_softmax_kernel<CAUSAL, 2>), dim3((unsigned)((nrow4 + 1) / 2)), dim3(UNT), 0, s, a);
+    else
+        hipLaunchKernelGGL((unfused_softmax_kernel<CAUSAL, 4>), dim3((unsigned)nrow4), dim3(UNT), 0, s, a);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((unfused_pv_kernel<TIN, TOUT, D, CAUSAL>), dim3((unsigned)npv), dim3(UNT), 0, s, a);

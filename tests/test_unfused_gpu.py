@@ -5,7 +5,8 @@ on the same seeded inputs as the fused path.
 Output and lse: every element within the tolerance rules of helpers.py (verify
 mode: fp32 output within 2e-3; shipped output within 2e-3 beyond its half
 ulp), on edge shapes (ragged rows and keys, Nk < 64, causal with Nq < Nk, Nq >
-Nk without a mask, group sizes 1, 2, 3, 4 and 16, both head sizes, negative
+Nk without a mask, group sizes 1, 2, 3, 4 and 16, both head sizes, rows
+held by one, two and four softmax waves and rows longer than that, negative
 and zero scales) and on the three prefill workloads at reduced sizes and at
 full size (in the launch configuration the benchmark times), every element.
 Intermediate results: the materialised weights P equal the oracle's
@@ -37,6 +38,9 @@ EDGE = [
     (1, 2, 2, 1, 1, 128, 1, "f16"),         # one key
     (1, 8, 8, 64, 64, 64, 1, "bf16"),       # exact tiles
     (1, 4, 1, 129, 129, 128, 1, "bf16"),    # one row past a 128-row workgroup
+    (1, 2, 1, 3, 6000, 64, 1, "f16"),       # softmax: two waves per row
+    (1, 2, 2, 40, 9000, 128, 1, "bf16"),    # softmax: four waves per row, one segment partly visible
+    (1, 2, 1, 2, 20000, 64, 0, "bf16"),     # softmax: four waves per row and a streamed tail
 ]
 
 
