@@ -299,8 +299,9 @@ __global__ __launch_bounds__(UNT) void unfused_softmax_kernel(UnfusedArgs a) {
 }
 
 // P.V: the workgroup's four slots share each staged V tile (the slot layout
-// of the scores kernel, longest rows first).  Each tile's P loads are issued
-// before the workgroup stages the V tile, so the two overlap.
+// of the scores kernel, longest rows first).  The next tile's V loads are in
+// flight during a tile's products; a tile's P loads go out at the start of
+// its step (the wait before the V copy into LDS also covers them).
 template <typename TIN, typename TOUT, int D, bool CAUSAL>
 __global__ __launch_bounds__(UNT) void unfused_pv_kernel(UnfusedArgs a) {
     constexpr int VS = D + 8;            // LDS row stride (fp16 elements)
