@@ -11,7 +11,12 @@ workloads are reported alongside.  The fp64 CPU oracle is timed on the host
 cores on the headline workload as a baseline (not a target), and the GPU
 output of the benchmark is checked against it.  The Q8_0 matrix-vector
 products of a decode step (the linear layers of a TinyLlama-1.1B shaped
-model) are reported under "q8_0_gemv" as weight GB/s.
+model) are reported under "q8_0_gemv" as weight GB/s.  Also reported: the
+inter-head packing ablation ("packing_ablation"), the fused kernel against
+the unfused self-attention path with its materialised score matrix
+("unfused_ablation"), decode against a paged cache ("paged_decode") and a
+chunked prefill against caches of per-sequence lengths, contiguous and
+paged ("chunked_prefill").
 
 Prints ONE JSON line on stdout; progress goes to stderr.
 """
