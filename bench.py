@@ -172,9 +172,7 @@ def unfused_vs_fused(torch, fa, w, steps):
                                                        scale=w.softmax_scale, out=out, lse=lse,
                                                        workspace=ws)], steps, 2)
     es = torch.finfo(DTYPES[w.dtype]).bits // 8
-    vis = w.B * w.Hq * w.visible_pairs()
-    io = (2 * w.B * w.Nq * w.Hq * w.D + 2 * w.B * w.Nk * w.Hkv * w.D) * es
-    nbytes = 12 * vis + io
+    nbytes = unfused_min_bytes(w.B, w.Hq, w.Hkv, w.Nq, w.Nk, w.D, w.visible_pairs(), es)
     del ws
     return {"workload": w.name, "fused_us": round(fused_ms * 1e3, 2),
             "unfused_us": round(unf_ms * 1e3, 2), "fused_speedup": round(unf_ms / fused_ms, 2),
@@ -242,6 +240,20 @@ def paged_decode(torch, fa, w, steps, warmup, page_size):
     return ms * 1e3, w.kv_bytes() / (ms * 1e-3) / 1e9
 
 
+def chunked_visible_pairs(Nq, lens):
+    """Visible (query, key) pairs per head of a causal chunked prefill: the
+    Nq queries of a sequence of length L are its last positions, so query i
+    sees L - Nq + i + 1 keys (L >= Nq)."""
+    return sum(Nq * (L - Nq + 1) + Nq * (Nq - 1) // 2 for L in lens)
+
+
+def unfused_min_bytes(B, Hq, Hkv, Nq, Nk, D, vis_per_head, esize):
+    """Minimum HBM bytes of the unfused path: per visible score, S written and
+    read in fp32 and P written and read in fp16; Q, K, V and O once."""
+    vis = B * Hq * vis_per_head
+    return 12 * vis + (2 * B * Nq * Hq * D + 2 * B * Nk * Hkv * D) * esize
+
+
 def chunked_prefill(torch, fa, steps, warmup):
     """Chunked prefill: 512 new query tokens per sequence against K/V caches
     whose valid lengths are 4096, 3072, 2048 and 1024 (the headline model's
@@ -253,7 +265,7 @@ def chunked_prefill(torch, fa, steps, warmup):
     B, Hq, Hkv, Nq, Nk, D, ps = 4, 32, 8, 512, 4096, 64, 256
     lens = [4096, 3072, 2048, 1024]
     q, k, v = make_qkv(B, Hq, Hkv, Nq, Nk, D, "bf16", seed=5000)
-    vis = sum(Nq * (L - Nq + 1) + Nq * (Nq - 1) // 2 for L in lens)
+    vis = chunked_visible_pairs(Nq, lens)
     flops = 4 * D * Hq * vis
     qd, kd, vd = q.cuda(), k.cuda(), v.cuda()
     sl = torch.tensor(lens, dtype=torch.int32, device="cuda")

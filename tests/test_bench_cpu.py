@@ -1,0 +1,35 @@
+"""Host-side checks of the benchmark's work counts (no GPU): the closed forms
+bench.py divides by are compared with brute-force counts on small shapes."""
+import itertools
+
+import bench
+from paper_2608_18656_amd.inputs import Workload
+
+
+def _brute_visible(Nq, L, causal=True):
+    # query i (the sequence's position L - Nq + i) sees key j iff j <= L - Nq + i
+    return sum(1 for i, j in itertools.product(range(Nq), range(L)) if not causal or j <= L - Nq + i)
+
+
+def test_chunked_visible_pairs_brute_force():
+    for Nq, lens in [(1, [1]), (3, [3, 7]), (5, [5, 9, 64]), (16, [16, 17, 100])]:
+        assert bench.chunked_visible_pairs(Nq, lens) == sum(_brute_visible(Nq, L) for L in lens)
+
+
+def test_workload_visible_pairs_brute_force():
+    for Nq, Nk, causal in [(1, 9, True), (7, 7, True), (5, 12, True), (6, 4, False), (13, 40, True)]:
+        w = Workload("t", 1, 2, 1, Nq, Nk, 64, causal, "f16", 0)
+        assert w.visible_pairs() == _brute_visible(Nq, Nk, causal)
+
+
+def test_unfused_min_bytes_counts_each_array_once():
+    B, Hq, Hkv, Nq, Nk, D, es = 2, 4, 2, 5, 9, 64, 2
+    w = Workload("t", B, Hq, Hkv, Nq, Nk, D, True, "f16", 0)
+    vis = B * Hq * w.visible_pairs()
+    s_bytes, p_bytes = 4 * vis, 2 * vis                  # S and P, each written once and read once
+    q_o = 2 * B * Nq * Hq * D * es                        # Q read, O written
+    k_v = 2 * B * Nk * Hkv * D * es                       # K and V read
+    assert bench.unfused_min_bytes(B, Hq, Hkv, Nq, Nk, D, w.visible_pairs(), es) == \
+        2 * s_bytes + 2 * p_bytes + q_o + k_v
+    # the headline workload: 12 x 67,141,632 visible scores + 20,971,520 bytes of Q, K, V, O
+    assert bench.unfused_min_bytes(1, 32, 8, 2048, 2048, 64, 2048 * 2049 // 2, 2) == 826_671_104
