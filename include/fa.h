@@ -222,9 +222,10 @@ fa_status_t fa_set_workspace(void *dev_ptr, size_t bytes);
  *              [B][Hq][Nq][NkP] fp16, NkP = Nk rounded up to 64, defined on
  *              each row's visible keys).  Calls sharing one workspace must be
  *              ordered.
- * fp16 / bf16 inputs with D in {64, 128} and Nk <= 2^23 only.  Errors: those
- * of fa_fwd, then FA_ERR_DTYPE for fp32 inputs, FA_ERR_HEAD_DIM for another D,
- * FA_ERR_DIM for Nk > 2^23, FA_ERR_NULL for a NULL workspace, FA_ERR_ALIGN
+ * fp16 / bf16 inputs with D in {64, 128}, Nk <= 2^23 and B * Hq * Nq < 2^31
+ * only.  Errors: those of fa_fwd, then FA_ERR_DTYPE for fp32 inputs,
+ * FA_ERR_HEAD_DIM for another D, FA_ERR_DIM for Nk > 2^23 or B * Hq * Nq >=
+ * 2^31, FA_ERR_NULL for a NULL workspace, FA_ERR_ALIGN
  * for a misaligned one, FA_ERR_DIM when the workspace size overflows, FA_ERR_WORKSPACE when workspace_bytes is too
  * small, FA_ERR_ALIAS when it overlaps a tensor; all before any HIP call. */
 fa_status_t fa_fwd_unfused(const void *q, const void *k, const void *v, void *o, float *lse,

@@ -329,6 +329,7 @@ fa_status_t fa_fwd_unfused(const void *q, const void *k, const void *v, void *o,
     if (in_dtype == FA_F32) return FA_ERR_DTYPE;
     if (!fa::unfused_supported(D, in_dtype)) return FA_ERR_HEAD_DIM;
     if (Nk > (1 << 23)) return FA_ERR_DIM;   // 32-bit offsets within a 32-row block of scores
+    if ((long long)B * Hq * Nq > 0x7fffffffLL) return FA_ERR_DIM;   // one softmax workgroup per row at most
     if (!workspace) return FA_ERR_NULL;
     if (reinterpret_cast<uintptr_t>(workspace) & 255) return FA_ERR_ALIGN;
     const size_t need = fa::unfused_workspace_bytes(B, Hq, Nq, Nk);

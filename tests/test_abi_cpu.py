@@ -221,3 +221,6 @@ def test_unfused_argument_errors_before_any_launch():
     assert call(ws=O - 256) == 8                           # workspace runs into o
     assert call(o=Q + 64) == 8                             # the checks of fa_fwd come first
     assert call(B=1, Hq=2, Hkv=1, Nq=1, Nk=(1 << 23) + 1) == 2   # 32-bit offsets in a block of scores
+    far = [k << 44 for k in range(1, 7)]                 # fake addresses that cannot overlap
+    assert call(*far[:5], B=1 << 10, Hq=1 << 11, Hkv=1 << 11, Nq=1 << 10, Nk=1 << 10, causal=0,
+                ws=far[5]) == 2                           # 2^31 rows of scores
