@@ -38,11 +38,21 @@
  * before any HIP call; device faults surface at the caller's next
  * synchronisation.  No exception crosses this interface.
  *
- * Decode needs a device workspace for the per-split partial results.  The
- * library owns one per device, grows it on demand (hipMalloc, which may
- * synchronise) and keeps it until fa_release_workspace(); make one warm-up
- * call before timing.  Calls on the same device share that workspace, so
- * concurrent calls on different streams of one device race: serialise them.
+ * Decode needs a device workspace for the per-split partial results
+ * (fa_workspace_bytes()).  There are three ways to provide it:
+ *  - the *_ws entry points take it with each call (caller-owned, checked
+ *    before any HIP call, never allocated by the library): calls running
+ *    concurrently on different streams each pass their own;
+ *  - otherwise the library owns one buffer per (device, stream), allocated on
+ *    first use and grown when a call needs more (make one warm-up call before
+ *    timing or graph capture: no buffer is allocated while the stream is
+ *    being captured, and such a call returns FA_ERR_WORKSPACE).  An outgrown
+ *    buffer is kept, not freed, until fa_release_workspace(), so that work
+ *    queued earlier and graphs captured earlier stay valid; calls on
+ *    different streams never share a buffer (the buffer of a stream is kept
+ *    after the stream is destroyed, again until fa_release_workspace());
+ *  - fa_set_workspace() installs one caller-owned buffer for a device, which
+ *    then serves every call on that device that does not pass its own.
  */
 #ifndef FA_H_
 #define FA_H_
@@ -70,7 +80,7 @@ typedef enum {
     FA_ERR_ALIGN = 7,        /* a tensor pointer is not 16-byte aligned */
     FA_ERR_ALIAS = 8,        /* o or lse overlaps q, k, v, or each other */
     FA_ERR_DTYPE = 9,        /* unknown dtype, or out_dtype not in {in_dtype, FA_F32} */
-    FA_ERR_WORKSPACE = 10,   /* workspace allocation failed, or the caller-set one is too small */
+    FA_ERR_WORKSPACE = 10,   /* workspace allocation failed or not allowed (stream capture), or a caller-owned one is too small */
     FA_ERR_HIP = 11,         /* a HIP runtime call or kernel launch failed */
     FA_ERR_SPLITS = 12,      /* num_splits outside [0, FA_MAX_SPLITS] */
     FA_ERR_PACKING = 13      /* heads_per_workgroup not 0, 1, 2 or 4, or not a divisor of Hq / Hkv */
@@ -187,8 +197,11 @@ fa_status_t fa_fwd_kvcache_paged(const void *q, const void *k_pages, const void 
 size_t fa_workspace_bytes(int B, int Hq, int Hkv, int Nq, int Nk, int D, fa_dtype_t in_dtype,
                           int num_splits);
 
-/* Frees the library-owned workspace of the current device (synchronises the
- * device first).  Safe to call when none is held. */
+/* Frees every library-owned workspace buffer of the current device (those of
+ * all its streams, and outgrown ones), after synchronising the device.  Safe
+ * to call when none is held.  Graphs captured with library-owned workspaces
+ * of this device must not be replayed afterwards.  Returns FA_ERR_HIP if the
+ * device cannot be read, synchronised or a buffer freed. */
 fa_status_t fa_release_workspace(void);
 
 /* Caller-owned decode workspace for the current device (the split-KV
@@ -200,12 +213,54 @@ fa_status_t fa_release_workspace(void);
  * cleared.  After a successful call every decode call on this device uses
  * it and never allocates; a call that needs more than `bytes` (see
  * fa_workspace_bytes) returns FA_ERR_WORKSPACE without launching anything.
- * Calls sharing one workspace must be ordered (one stream, or synchronised
- * streams).  fa_set_workspace(NULL, 0) returns the device to the
- * library-owned workspace.  Errors: FA_ERR_NULL for a NULL pointer with
+ * Every call on the device that does not pass its own workspace shares this
+ * one, so such calls must be ordered (one stream, or synchronised streams);
+ * concurrent streams should use the *_ws entry points instead.
+ * fa_set_workspace(NULL, 0) returns the device to the library-owned
+ * per-stream workspaces.  Errors: FA_ERR_NULL for a NULL pointer with
  * bytes > 0 or a non-NULL pointer with bytes == 0, FA_ERR_ALIGN for a
  * misaligned pointer, FA_ERR_HIP when the current device cannot be read. */
 fa_status_t fa_set_workspace(void *dev_ptr, size_t bytes);
+
+/* The forward with a caller-owned decode workspace passed with the call (the
+ * split-KV partial results of Sec. 4.1's one-row decode, merged by their
+ * log-sum-exp): otherwise fa_fwd_splitkv (num_splits as there).  Calls that
+ * take no split-KV path (prefill, fp32, other D) ignore the workspace, which
+ * may then be NULL.
+ *   workspace        device memory on the current device, 16-byte aligned,
+ *                    owned by the caller; at least workspace_bytes long
+ *   workspace_bytes  its size; the call needs fa_workspace_bytes(B, Hq, Hkv,
+ *                    Nq, Nk, D, in_dtype, num_splits)
+ * The library never allocates for these calls and uses the workspace only as
+ * scratch during the call's kernels; calls running concurrently (e.g. on
+ * different streams) must pass disjoint workspaces.  Errors (before any HIP
+ * call), on the split-KV path: FA_ERR_NULL for a NULL workspace,
+ * FA_ERR_ALIGN for a misaligned one, FA_ERR_WORKSPACE when workspace_bytes is
+ * too small, FA_ERR_ALIAS when it overlaps q, k, v, o or lse; otherwise as
+ * fa_fwd_splitkv. */
+fa_status_t fa_fwd_ws(const void *q, const void *k, const void *v, void *o, float *lse, int B,
+                      int Hq, int Hkv, int Nq, int Nk, int D, int causal, float scale, void *stream,
+                      fa_dtype_t in_dtype, fa_dtype_t out_dtype, int num_splits, void *workspace,
+                      size_t workspace_bytes);
+
+/* fa_fwd_kvcache with a caller-owned decode workspace passed with the call
+ * (fa_workspace_bytes(B, Hq, Hkv, Nq, Nk, D, in_dtype, 0) bytes; semantics
+ * and errors of the workspace as for fa_fwd_ws). */
+fa_status_t fa_fwd_kvcache_ws(const void *q, const void *k, const void *v, void *o, float *lse,
+                              const int *seqlens_k, int B, int Hq, int Hkv, int Nq, int Nk, int D,
+                              int causal, float scale, void *stream, fa_dtype_t in_dtype,
+                              fa_dtype_t out_dtype, void *workspace, size_t workspace_bytes);
+
+/* fa_fwd_kvcache_paged with a caller-owned decode workspace passed with the
+ * call (fa_workspace_bytes(B, Hq, Hkv, 1, page_size * max_pages, D,
+ * in_dtype, 0) bytes for decode; semantics and errors of the workspace as for
+ * fa_fwd_ws). */
+fa_status_t fa_fwd_kvcache_paged_ws(const void *q, const void *k_pages, const void *v_pages, void *o,
+                                    float *lse, const int *seqlens_k, const int *block_table, int B,
+                                    int Hq, int Hkv, int Nq, int D, int page_size, int max_pages,
+                                    int num_pages, int causal, float scale, void *stream,
+                                    fa_dtype_t in_dtype, fa_dtype_t out_dtype, void *workspace,
+                                    size_t workspace_bytes);
 
 /* Unfused self-attention: the same result as fa_fwd, computed the way the
  * paper's optimised self-attention does it (Sec. 4.2), with the score matrix

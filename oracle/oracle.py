@@ -209,11 +209,17 @@ def attention_parallel(q, k, v, causal: bool, scale: float, workers: int = 1,
 
 
 def default_workers() -> int:
+    """Worker processes for the row fan-out: the CPUs this process may run on
+    (its affinity mask), limited by OMP_NUM_THREADS where the environment sets
+    a CPU share that way."""
     try:
         n = len(os.sched_getaffinity(0))
     except AttributeError:  # pragma: no cover
         n = os.cpu_count() or 1
-    return max(1, min(n, 16))
+    share = os.environ.get("OMP_NUM_THREADS", "")
+    if share.isdigit() and int(share) > 0:
+        n = min(n, int(share))
+    return max(1, n)
 
 
 __all__: Iterable[str] = ["build", "attention", "attention_rows", "attention_parallel",

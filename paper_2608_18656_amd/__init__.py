@@ -69,9 +69,18 @@ def _prepare(q, k, v, out, lse, out_dtype, return_lse):
     return (B, Hq, Hkv, Nq, Nk, D), out, lse, odt
 
 
+def _workspace_arg(workspace, device):
+    """(pointer, bytes) of a caller-owned decode workspace tensor."""
+    torch = _torch()
+    if (workspace.dtype != torch.uint8 or not workspace.is_contiguous()
+            or workspace.device != device):
+        raise ValueError("workspace must be a contiguous uint8 tensor on q's device")
+    return workspace.data_ptr(), workspace.numel()
+
+
 def fwd(q, k, v, causal: bool = False, scale: float | None = None, out=None, lse=None,
         out_dtype=None, return_lse: bool = True, num_splits: int | None = None,
-        heads_per_workgroup: int | None = None):
+        heads_per_workgroup: int | None = None, workspace=None):
     """Attention forward o = softmax(scale * q k^T) v on the GPU.
 
     q [B, Nq, Hq, D], k and v [B, Nk, Hkv, D] (contiguous, same dtype and
@@ -81,7 +90,10 @@ def fwd(q, k, v, causal: bool = False, scale: float | None = None, out=None, lse
     ``out_dtype=torch.float32`` returns the kernel's fp32 result before the
     final rounding.  ``num_splits`` forces the decode split count (decode
     shapes only); ``heads_per_workgroup`` (1, 2 or 4) forces the prefill
-    query-head packing (see fa_fwd_packed).  Returns (out, lse) with lse
+    query-head packing (see fa_fwd_packed).  ``workspace`` (a contiguous uint8
+    GPU tensor of at least workspace_bytes(...) bytes) is this call's own
+    decode workspace (fa_fwd_ws); otherwise the library-owned one of the
+    current stream is used.  Returns (out, lse) with lse
     [B, Hq, Nq] float32 natural-log
     log-sum-exp (None if return_lse is False and no lse tensor was given).
     """
@@ -98,9 +110,11 @@ def fwd(q, k, v, causal: bool = False, scale: float | None = None, out=None, lse
             lse.data_ptr() if lse is not None else None, B, Hq, Hkv, Nq, Nk, D,
             int(bool(causal)), float(scale), stream, codes[q.dtype], codes.get(odt, -1))
     with torch.cuda.device(q.device):
-        if num_splits is not None and heads_per_workgroup is not None:
-            raise ValueError("num_splits and heads_per_workgroup are exclusive")
-        if num_splits is not None:
+        if heads_per_workgroup is not None and (num_splits is not None or workspace is not None):
+            raise ValueError("heads_per_workgroup excludes num_splits and workspace")
+        if workspace is not None:
+            st = lib.fa_fwd_ws(*args, int(num_splits or 0), *_workspace_arg(workspace, q.device))
+        elif num_splits is not None:
             st = lib.fa_fwd_splitkv(*args, int(num_splits))
         elif heads_per_workgroup is not None:
             st = lib.fa_fwd_packed(*args, int(heads_per_workgroup))
@@ -153,12 +167,13 @@ def fwd_unfused(q, k, v, causal: bool = False, scale: float | None = None, out=N
 
 
 def fwd_kvcache(q, k_cache, v_cache, seqlens_k, causal: bool = False, scale: float | None = None,
-                out=None, lse=None, out_dtype=None, return_lse: bool = True):
+                out=None, lse=None, out_dtype=None, return_lse: bool = True, workspace=None):
     """Attention against K/V caches [B, Nk, Hkv, D] of which the first
     ``seqlens_k[b]`` rows are valid (``seqlens_k``: int32 [B] on the same
     device); q [B, Nq, Hq, D] holds each sequence's last Nq positions (decode
     for Nq = 1, chunked prefill otherwise).  Rows that see no key give 0 and
-    lse -inf.  See fa_fwd_kvcache in include/fa.h."""
+    lse -inf.  ``workspace``: this call's own decode workspace (uint8 GPU
+    tensor; fa_fwd_kvcache_ws).  See fa_fwd_kvcache in include/fa.h."""
     from . import _lib
 
     lib = _lib.load()
@@ -172,23 +187,29 @@ def fwd_kvcache(q, k_cache, v_cache, seqlens_k, causal: bool = False, scale: flo
         scale = 1.0 / math.sqrt(D)
     codes = _codes()
     stream = torch.cuda.current_stream(q.device).cuda_stream
+    args = (q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), out.data_ptr(),
+            lse.data_ptr() if lse is not None else None, seqlens_k.data_ptr(),
+            B, Hq, Hkv, Nq, Nk, D, int(bool(causal)), float(scale), stream,
+            codes[q.dtype], codes.get(odt, -1))
     with torch.cuda.device(q.device):
-        st = lib.fa_fwd_kvcache(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), out.data_ptr(),
-                                lse.data_ptr() if lse is not None else None, seqlens_k.data_ptr(),
-                                B, Hq, Hkv, Nq, Nk, D, int(bool(causal)), float(scale), stream,
-                                codes[q.dtype], codes.get(odt, -1))
+        if workspace is not None:
+            st = lib.fa_fwd_kvcache_ws(*args, *_workspace_arg(workspace, q.device))
+        else:
+            st = lib.fa_fwd_kvcache(*args)
     _check(lib, st)
     return out, lse
 
 
 def fwd_kvcache_paged(q, k_pages, v_pages, block_table, seqlens_k, causal: bool = False,
                       scale: float | None = None, out=None, lse=None, out_dtype=None,
-                      return_lse: bool = True):
+                      return_lse: bool = True, workspace=None):
     """Attention against a paged K/V cache: ``k_pages``, ``v_pages``
     [num_pages, page_size, Hkv, D] (page_size a multiple of 64), ``block_table``
     int32 [B, max_pages] (page of each block of page_size keys of each
     sequence), ``seqlens_k`` int32 [B]; q [B, Nq, Hq, D] holds each sequence's
-    last Nq positions.  See fa_fwd_kvcache_paged in include/fa.h."""
+    last Nq positions.  ``workspace``: this call's own decode workspace
+    (uint8 GPU tensor; fa_fwd_kvcache_paged_ws).  See fa_fwd_kvcache_paged in
+    include/fa.h."""
     from . import _lib
 
     lib = _lib.load()
@@ -228,12 +249,15 @@ def fwd_kvcache_paged(q, k_pages, v_pages, block_table, seqlens_k, causal: bool 
         scale = 1.0 / math.sqrt(D)
     codes = _codes()
     stream = torch.cuda.current_stream(q.device).cuda_stream
-    with torch.cuda.device(q.device):
-        st = lib.fa_fwd_kvcache_paged(
-            q.data_ptr(), k_pages.data_ptr(), v_pages.data_ptr(), out.data_ptr(),
+    args = (q.data_ptr(), k_pages.data_ptr(), v_pages.data_ptr(), out.data_ptr(),
             lse.data_ptr() if lse is not None else None, seqlens_k.data_ptr(), block_table.data_ptr(),
             B, Hq, Hkv, Nq, D, page_size, max_pages, num_pages, int(bool(causal)), float(scale),
             stream, codes[q.dtype], codes.get(odt, -1))
+    with torch.cuda.device(q.device):
+        if workspace is not None:
+            st = lib.fa_fwd_kvcache_paged_ws(*args, *_workspace_arg(workspace, q.device))
+        else:
+            st = lib.fa_fwd_kvcache_paged(*args)
     _check(lib, st)
     return out, lse
 

@@ -5,6 +5,7 @@
 #include <cmath>
 #include <cstdint>
 #include <mutex>
+#include <vector>
 
 #include "../../include/fa.h"
 #include "fa_internal.h"
@@ -24,48 +25,79 @@ bool mul_ok(long long a, long long b, long long *r) {
     return true;
 }
 
-// Device workspace for the split-KV partial results (one per device):
-// library-owned and grow-only, unless the caller has set its own.
-struct Workspace {
-    void *ptr = nullptr;
-    size_t bytes = 0;
-    void *user = nullptr;       // caller-owned workspace (fa_set_workspace), or NULL
-    size_t user_bytes = 0;
+// Device workspace for the split-KV partial results.  Library-owned buffers
+// are kept per (device, stream), so that calls on different streams never
+// share one; a buffer that is outgrown is retired, not freed (an earlier call
+// or a captured graph may still use it) until fa_release_workspace().  No
+// buffer is allocated while the stream is being captured.  A caller-owned
+// workspace set with fa_set_workspace() replaces them for its device.
+struct OwnedWs {
+    int dev;
+    hipStream_t stream;
+    void *ptr;
+    size_t bytes;
+};
+struct Retired {
+    int dev;
+    void *ptr;
 };
 constexpr int kMaxDevices = 64;
-Workspace g_ws[kMaxDevices];
+struct UserWs {
+    void *ptr = nullptr;
+    size_t bytes = 0;
+};
+UserWs g_user[kMaxDevices];
+std::vector<OwnedWs> g_owned;
+std::vector<Retired> g_retired;
 std::mutex g_ws_mu;
 
-fa_status_t get_workspace(size_t need, void **out, bool *user) {
+fa_status_t get_workspace(size_t need, hipStream_t stream, void **out, bool *user) {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return FA_ERR_HIP;
     std::lock_guard<std::mutex> lk(g_ws_mu);
-    Workspace &w = g_ws[dev];
-    *user = w.user != nullptr;
-    if (w.user) {
-        if (w.user_bytes < need) return FA_ERR_WORKSPACE;
-        *out = w.user;
+    *user = g_user[dev].ptr != nullptr;
+    if (*user) {
+        if (g_user[dev].bytes < need) return FA_ERR_WORKSPACE;
+        *out = g_user[dev].ptr;
         return FA_OK;
     }
-    if (w.bytes < need) {
-        if (w.ptr) {
-            // earlier calls may still be reading the old buffer
-            if (hipDeviceSynchronize() != hipSuccess) return FA_ERR_HIP;
-            if (hipFree(w.ptr) != hipSuccess) return FA_ERR_HIP;
-            w.ptr = nullptr;
-            w.bytes = 0;
-        }
-        size_t sz = need < ((size_t)1 << 20) ? ((size_t)1 << 20) : need;
-        if (hipMalloc(&w.ptr, sz) != hipSuccess) {
-            w.ptr = nullptr;
-            (void)hipGetLastError();
-            return FA_ERR_WORKSPACE;
-        }
-        w.bytes = sz;
+    OwnedWs *cur = nullptr;
+    for (OwnedWs &w : g_owned)
+        if (w.dev == dev && w.stream == stream) cur = &w;
+    if (cur && cur->bytes >= need) {
+        *out = cur->ptr;
+        return FA_OK;
     }
-    *out = w.ptr;
+    // a new buffer is needed: never inside stream capture (the allocation
+    // would invalidate it)
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(stream, &cs) != hipSuccess) {
+        (void)hipGetLastError();
+        return FA_ERR_WORKSPACE;
+    }
+    if (cs != hipStreamCaptureStatusNone) return FA_ERR_WORKSPACE;
+    const size_t sz = need < ((size_t)1 << 20) ? ((size_t)1 << 20) : need;
+    void *ptr = nullptr;
+    if (hipMalloc(&ptr, sz) != hipSuccess) {
+        (void)hipGetLastError();
+        return FA_ERR_WORKSPACE;
+    }
+    if (cur) {
+        g_retired.push_back(Retired{dev, cur->ptr});
+        cur->ptr = ptr;
+        cur->bytes = sz;
+    } else {
+        g_owned.push_back(OwnedWs{dev, stream, ptr, sz});
+    }
+    *out = ptr;
     return FA_OK;
 }
+
+// A caller-owned workspace passed with one call (the *_ws entry points).
+struct CallWs {
+    void *ptr;
+    size_t bytes;
+};
 
 // The argument checks of every attention entry point.  kv_rows: rows of
 // Hkv * D elements that k and v each hold (-1: B * Nk, the contiguous layout).
@@ -109,7 +141,8 @@ struct Paging {
 fa_status_t run(const void *q, const void *k, const void *v, void *o, float *lse, int B, int Hq,
                 int Hkv, int Nq, int Nk, int D, int causal, float scale, void *stream,
                 fa_dtype_t in, fa_dtype_t out, int splits_req, int hw_req = 0,
-                const int *seqlens = nullptr, const Paging &pg = Paging()) {
+                const int *seqlens = nullptr, const Paging &pg = Paging(),
+                const CallWs *cws = nullptr) {
     const long long kv_rows = pg.block_table ? (long long)pg.num_pages * pg.page_size : -1;
     fa_status_t st = validate_core(q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, in, out, kv_rows);
     if (st != FA_OK) return st;
@@ -126,8 +159,16 @@ fa_status_t run(const void *q, const void *k, const void *v, void *o, float *lse
         const size_t need = fa::decode_workspace_bytes(B, Hq, D, S);
         void *ws = nullptr;
         bool user = false;
-        st = get_workspace(need, &ws, &user);
-        if (st != FA_OK) return st;
+        if (cws) {   // this call's own workspace: checked here, never allocated
+            if (!cws->ptr) return FA_ERR_NULL;
+            if (reinterpret_cast<uintptr_t>(cws->ptr) & 15) return FA_ERR_ALIGN;
+            if (cws->bytes < need) return FA_ERR_WORKSPACE;
+            ws = cws->ptr;
+            user = true;
+        } else {
+            st = get_workspace(need, s, &ws, &user);
+            if (st != FA_OK) return st;
+        }
         if (user) {   // a caller-owned workspace must not overlap the call's tensors
             const size_t qb = (size_t)B * Nq * Hq * D * esize(in);
             const size_t kb = (size_t)(kv_rows < 0 ? (long long)B * Nk : kv_rows) * Hkv * D * esize(in);
@@ -162,7 +203,7 @@ const char *fa_status_string(fa_status_t s) {
     case FA_ERR_ALIAS: return "FA_ERR_ALIAS: o or lse overlaps another tensor";
     case FA_ERR_DTYPE: return "FA_ERR_DTYPE: unsupported dtype combination";
     case FA_ERR_WORKSPACE:
-        return "FA_ERR_WORKSPACE: workspace allocation failed, or the caller-set workspace is too small";
+        return "FA_ERR_WORKSPACE: workspace allocation failed or not allowed during stream capture, or a caller-owned workspace is too small";
     case FA_ERR_HIP: return "FA_ERR_HIP: HIP runtime or launch error";
     case FA_ERR_SPLITS: return "FA_ERR_SPLITS: num_splits out of range";
     case FA_ERR_PACKING:
@@ -221,10 +262,14 @@ fa_status_t fa_fwd_packed(const void *q, const void *k, const void *v, void *o, 
                0, heads_per_workgroup);
 }
 
-fa_status_t fa_fwd_kvcache(const void *q, const void *k, const void *v, void *o, float *lse,
-                           const int *seqlens_k, int B, int Hq, int Hkv, int Nq, int Nk, int D,
-                           int causal, float scale, void *stream, fa_dtype_t in_dtype,
-                           fa_dtype_t out_dtype) {
+}  // extern "C"
+
+namespace {
+
+fa_status_t kvcache(const void *q, const void *k, const void *v, void *o, float *lse,
+                    const int *seqlens_k, int B, int Hq, int Hkv, int Nq, int Nk, int D, int causal,
+                    float scale, void *stream, fa_dtype_t in_dtype, fa_dtype_t out_dtype,
+                    const CallWs *cws) {
     if (!seqlens_k) return FA_ERR_NULL;
     if (reinterpret_cast<uintptr_t>(seqlens_k) & 3) return FA_ERR_ALIGN;
     if (B >= 1 && o && Hq >= 1 && Nq >= 1 && D >= 1) {
@@ -234,14 +279,14 @@ fa_status_t fa_fwd_kvcache(const void *q, const void *k, const void *v, void *o,
             return FA_ERR_ALIAS;
     }
     return run(q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, stream, in_dtype, out_dtype, 0,
-               0, seqlens_k);
+               0, seqlens_k, Paging(), cws);
 }
 
-fa_status_t fa_fwd_kvcache_paged(const void *q, const void *k_pages, const void *v_pages, void *o,
-                                 float *lse, const int *seqlens_k, const int *block_table, int B,
-                                 int Hq, int Hkv, int Nq, int D, int page_size, int max_pages,
-                                 int num_pages, int causal, float scale, void *stream,
-                                 fa_dtype_t in_dtype, fa_dtype_t out_dtype) {
+fa_status_t kvcache_paged(const void *q, const void *k_pages, const void *v_pages, void *o,
+                          float *lse, const int *seqlens_k, const int *block_table, int B, int Hq,
+                          int Hkv, int Nq, int D, int page_size, int max_pages, int num_pages,
+                          int causal, float scale, void *stream, fa_dtype_t in_dtype,
+                          fa_dtype_t out_dtype, const CallWs *cws) {
     if (!seqlens_k || !block_table) return FA_ERR_NULL;
     if (page_size < 64 || page_size % 64 != 0 || max_pages < 1 || num_pages < 1 ||
         (long long)page_size * max_pages > 0x7fffffffLL || (long long)B * max_pages > 0x7fffffffLL)
@@ -274,7 +319,59 @@ fa_status_t fa_fwd_kvcache_paged(const void *q, const void *k_pages, const void 
     pg.max_pages = max_pages;
     pg.num_pages = num_pages;
     return run(q, k_pages, v_pages, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, stream, in_dtype,
-               out_dtype, 0, 0, seqlens_k, pg);
+               out_dtype, 0, 0, seqlens_k, pg, cws);
+}
+
+}  // namespace
+
+extern "C" {
+
+fa_status_t fa_fwd_kvcache(const void *q, const void *k, const void *v, void *o, float *lse,
+                           const int *seqlens_k, int B, int Hq, int Hkv, int Nq, int Nk, int D,
+                           int causal, float scale, void *stream, fa_dtype_t in_dtype,
+                           fa_dtype_t out_dtype) {
+    return kvcache(q, k, v, o, lse, seqlens_k, B, Hq, Hkv, Nq, Nk, D, causal, scale, stream, in_dtype,
+                   out_dtype, nullptr);
+}
+
+fa_status_t fa_fwd_kvcache_paged(const void *q, const void *k_pages, const void *v_pages, void *o,
+                                 float *lse, const int *seqlens_k, const int *block_table, int B,
+                                 int Hq, int Hkv, int Nq, int D, int page_size, int max_pages,
+                                 int num_pages, int causal, float scale, void *stream,
+                                 fa_dtype_t in_dtype, fa_dtype_t out_dtype) {
+    return kvcache_paged(q, k_pages, v_pages, o, lse, seqlens_k, block_table, B, Hq, Hkv, Nq, D,
+                         page_size, max_pages, num_pages, causal, scale, stream, in_dtype, out_dtype,
+                         nullptr);
+}
+
+fa_status_t fa_fwd_ws(const void *q, const void *k, const void *v, void *o, float *lse, int B,
+                      int Hq, int Hkv, int Nq, int Nk, int D, int causal, float scale, void *stream,
+                      fa_dtype_t in_dtype, fa_dtype_t out_dtype, int num_splits, void *workspace,
+                      size_t workspace_bytes) {
+    const CallWs cws{workspace, workspace_bytes};
+    return run(q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, stream, in_dtype, out_dtype,
+               num_splits, 0, nullptr, Paging(), &cws);
+}
+
+fa_status_t fa_fwd_kvcache_ws(const void *q, const void *k, const void *v, void *o, float *lse,
+                              const int *seqlens_k, int B, int Hq, int Hkv, int Nq, int Nk, int D,
+                              int causal, float scale, void *stream, fa_dtype_t in_dtype,
+                              fa_dtype_t out_dtype, void *workspace, size_t workspace_bytes) {
+    const CallWs cws{workspace, workspace_bytes};
+    return kvcache(q, k, v, o, lse, seqlens_k, B, Hq, Hkv, Nq, Nk, D, causal, scale, stream, in_dtype,
+                   out_dtype, &cws);
+}
+
+fa_status_t fa_fwd_kvcache_paged_ws(const void *q, const void *k_pages, const void *v_pages, void *o,
+                                    float *lse, const int *seqlens_k, const int *block_table, int B,
+                                    int Hq, int Hkv, int Nq, int D, int page_size, int max_pages,
+                                    int num_pages, int causal, float scale, void *stream,
+                                    fa_dtype_t in_dtype, fa_dtype_t out_dtype, void *workspace,
+                                    size_t workspace_bytes) {
+    const CallWs cws{workspace, workspace_bytes};
+    return kvcache_paged(q, k_pages, v_pages, o, lse, seqlens_k, block_table, B, Hq, Hkv, Nq, D,
+                         page_size, max_pages, num_pages, causal, scale, stream, in_dtype, out_dtype,
+                         &cws);
 }
 
 size_t fa_workspace_bytes(int B, int Hq, int Hkv, int Nq, int Nk, int D, fa_dtype_t in_dtype,
@@ -292,8 +389,8 @@ fa_status_t fa_set_workspace(void *dev_ptr, size_t bytes) {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return FA_ERR_HIP;
     std::lock_guard<std::mutex> lk(g_ws_mu);
-    g_ws[dev].user = dev_ptr;
-    g_ws[dev].user_bytes = bytes;
+    g_user[dev].ptr = dev_ptr;
+    g_user[dev].bytes = bytes;
     return FA_OK;
 }
 
@@ -351,14 +448,26 @@ fa_status_t fa_release_workspace(void) {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return FA_ERR_HIP;
     std::lock_guard<std::mutex> lk(g_ws_mu);
-    Workspace &w = g_ws[dev];
-    if (w.ptr) {
-        if (hipDeviceSynchronize() != hipSuccess) return FA_ERR_HIP;
-        if (hipFree(w.ptr) != hipSuccess) return FA_ERR_HIP;
+    bool any = false;
+    for (const OwnedWs &w : g_owned) any = any || w.dev == dev;
+    for (const Retired &r : g_retired) any = any || r.dev == dev;
+    if (!any) return FA_OK;
+    // calls queued on any stream may still use these buffers
+    if (hipDeviceSynchronize() != hipSuccess) return FA_ERR_HIP;
+    fa_status_t st = FA_OK;
+    std::vector<OwnedWs> keep;
+    for (const OwnedWs &w : g_owned) {
+        if (w.dev != dev) keep.push_back(w);
+        else if (hipFree(w.ptr) != hipSuccess) st = FA_ERR_HIP;
     }
-    w.ptr = nullptr;
-    w.bytes = 0;
-    return FA_OK;
+    g_owned.swap(keep);
+    std::vector<Retired> keep_r;
+    for (const Retired &r : g_retired) {
+        if (r.dev != dev) keep_r.push_back(r);
+        else if (hipFree(r.ptr) != hipSuccess) st = FA_ERR_HIP;
+    }
+    g_retired.swap(keep_r);
+    return st;
 }
 
 }  // extern "C"

@@ -224,3 +224,44 @@ def test_unfused_argument_errors_before_any_launch():
     far = [k << 44 for k in range(1, 7)]                 # fake addresses that cannot overlap
     assert call(*far[:5], B=1 << 10, Hq=1 << 11, Hkv=1 << 11, Nq=1 << 10, Nk=1 << 10, causal=0,
                 ws=far[5]) == 2                           # 2^31 rows of scores
+
+
+def test_per_call_workspace_argument_errors_before_any_launch():
+    """fa_fwd_ws / fa_fwd_kvcache_ws / fa_fwd_kvcache_paged_ws: a decode call's
+    own workspace is checked (NULL, alignment, size, overlap) before any HIP
+    call, after the checks of the call it extends (fake addresses)."""
+    lib = _lib.load()
+    Q, K, V, O, L, S, T, W = (k << 32 for k in range(1, 9))
+    F16, BF16 = _lib.FA_F16, _lib.FA_BF16
+    B, Hq, Hkv, Nk, D = 16, 32, 8, 8192, 128
+    need = lib.fa_workspace_bytes(B, Hq, Hkv, 1, Nk, D, BF16, 0)
+    assert need > 0 and need == lib.fa_workspace_bytes(B, Hq, Hkv, 1, Nk, D, BF16, 2)   # 2 splits
+    assert lib.fa_workspace_bytes(B, Hq, Hkv, 1, Nk, D, BF16, 5) == B * Hq * 5 * (D + 2) * 4
+    assert lib.fa_workspace_bytes(1, 4, 2, 64, 64, 64, F16, 0) == 0   # prefill takes none
+
+    def fwd(ws=W, wsb=None, q=Q, o=O, Nq=1, splits=0, causal=0):
+        return lib.fa_fwd_ws(q, K, V, o, L, B, Hq, Hkv, Nq, Nk, D, causal, 0.088, None, BF16, BF16,
+                             splits, ws, need if wsb is None else wsb)
+
+    assert fwd(ws=None) == 1                       # decode needs a workspace
+    assert fwd(ws=W + 8) == 7                      # not 16-byte aligned
+    assert fwd(wsb=need - 1) == 10                 # too small
+    assert fwd(ws=K + 4096) == 8                   # inside k
+    assert fwd(ws=O - 64) == 8                     # runs into o
+    assert fwd(q=None) == 1 and fwd(splits=257) == 12   # the checks of fa_fwd_splitkv come first
+    assert fwd(splits=5, wsb=need) == 10           # 5 splits need more than the default 2
+
+    def kv(ws=W, wsb=None, sl=S):
+        return lib.fa_fwd_kvcache_ws(Q, K, V, O, L, sl, B, Hq, Hkv, 1, Nk, D, 0, 0.088, None, BF16, BF16,
+                                     ws, need if wsb is None else wsb)
+
+    assert kv(ws=None) == 1 and kv(ws=W + 4) == 7 and kv(wsb=16) == 10 and kv(ws=V) == 8
+    assert kv(sl=None) == 1                        # the lengths are checked first
+
+    def paged(ws=W, wsb=None, bt=T):
+        ps, mp, npg = 256, Nk // 256, B * (Nk // 256)
+        return lib.fa_fwd_kvcache_paged_ws(Q, K, V, O, L, S, bt, B, Hq, Hkv, 1, D, ps, mp, npg, 0, 0.088,
+                                           None, BF16, BF16, ws, need if wsb is None else wsb)
+
+    assert paged(ws=None) == 1 and paged(ws=W + 2) == 7 and paged(wsb=need - 16) == 10
+    assert paged(ws=O) == 8 and paged(bt=None) == 1

@@ -62,6 +62,45 @@ def test_weight_rows_sum_to_one(causal):
 
 
 @pytest.mark.parametrize("causal", [False, True])
+def test_weights_against_torch_softmax(causal):
+    """The weight entry point against torch's float64 softmax of the scaled
+    scores with an explicit bottom-right mask, per query head on its key/value
+    head h // G (catches a wrong scale, a wrong head map or mask, or an
+    unnormalised row in the weights the unfused path is checked against)."""
+    import torch
+
+    B, Hq, Hkv, Nq, Nk, D, scale = 2, 6, 2, 5, 8, 3, 0.8
+    q, k, v = qkv(B, Hq, Hkv, Nq, Nk, D, seed=21)
+    w = oracle.weights(q, k, v, causal, scale)
+    G = Hq // Hkv
+    qt, kt = torch.from_numpy(q), torch.from_numpy(k)
+    for b in range(B):
+        for h in range(Hq):
+            s = (qt[b, :, h, :] @ kt[b, :, h // G, :].T) * scale          # [Nq, Nk]
+            if causal:
+                i = torch.arange(Nq)[:, None]
+                j = torch.arange(Nk)[None, :]
+                s = s.masked_fill(j > i + (Nk - Nq), float("-inf"))
+            ref = torch.softmax(s, dim=-1).numpy()
+            np.testing.assert_allclose(w[b, h], ref, rtol=0, atol=1e-13)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_weights_times_values_is_the_output(causal):
+    """sum_j w_ij v_j equals the attention output of the other entry point
+    (catches the two entry points disagreeing on the head map, the mask or the
+    normalisation)."""
+    B, Hq, Hkv, Nq, Nk, D, scale = 2, 4, 2, 6, 7, 5, 1.1
+    q, k, v = qkv(B, Hq, Hkv, Nq, Nk, D, seed=22)
+    w = oracle.weights(q, k, v, causal, scale)
+    o, _ = oracle.attention(q, k, v, causal, scale)
+    G = Hq // Hkv
+    for b in range(B):
+        for h in range(Hq):
+            np.testing.assert_allclose(w[b, h] @ v[b, :, h // G, :], o[b, :, h, :], rtol=0, atol=1e-13)
+
+
+@pytest.mark.parametrize("causal", [False, True])
 def test_all_ones_values(causal):
     """V = 1 gives O = 1 for every row (catches missing division by l)."""
     q, k, _ = qkv(1, 3, 1, 6, 8, 4, seed=5)
