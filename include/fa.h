@@ -243,6 +243,24 @@ fa_status_t fa_fwd_ws(const void *q, const void *k, const void *v, void *o, floa
                       fa_dtype_t in_dtype, fa_dtype_t out_dtype, int num_splits, void *workspace,
                       size_t workspace_bytes);
 
+/* For callers that cannot allocate (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): fa_fwd_splitkv whose
+ * split-KV partial results go to a fixed device array inside the library
+ * (32 MiB, one copy per GPU, held until the process ends) instead of a
+ * workspace; it calls no hipMalloc, hipFree or other allocating routine.  The
+ * first call on a device reads that array's device address (a HIP query; the
+ * runtime places the array in that device's memory then, once), later calls
+ * touch no allocator at all.  Every call on one GPU shares its array, so calls that overlap
+ * on one GPU (e.g. on two streams) race: order them.  Errors: those of
+ * fa_fwd_splitkv, then FA_ERR_WORKSPACE (before any HIP call) when the
+ * partial results, fa_workspace_bytes(B, Hq, Hkv, Nq, Nk, D, in_dtype,
+ * num_splits), exceed 32 MiB, and FA_ERR_HIP when the array's address cannot
+ * be read.  Calls that take no split-KV path behave as fa_fwd_splitkv. */
+fa_status_t fa_fwd_splitkv_noalloc(const void *q, const void *k, const void *v, void *o, float *lse,
+                                   int B, int Hq, int Hkv, int Nq, int Nk, int D, int causal,
+                                   float scale, void *stream, fa_dtype_t in_dtype,
+                                   fa_dtype_t out_dtype, int num_splits);
+
 /* fa_fwd_kvcache with a caller-owned decode workspace passed with the call
  * (fa_workspace_bytes(B, Hq, Hkv, Nq, Nk, D, in_dtype, 0) bytes; semantics
  * and errors of the workspace as for fa_fwd_ws). */

@@ -8,7 +8,7 @@ from __future__ import annotations
 
 import math
 
-__all__ = ["fwd", "fwd_splitkv", "fwd_kvcache", "fwd_kvcache_paged", "fwd_unfused",
+__all__ = ["fwd", "fwd_splitkv", "fwd_splitkv_noalloc", "fwd_kvcache", "fwd_kvcache_paged", "fwd_unfused",
            "unfused_workspace_bytes", "q8_0_gemv", "FaError", "validate", "workspace_bytes", "release_workspace",
            "set_workspace", "version", "DTYPE_CODES"]
 
@@ -296,6 +296,31 @@ def q8_0_gemv(w, x, out=None, out_dtype=None):
                               codes.get(odt, -1), stream)
     _check(lib, st)
     return out
+
+
+def fwd_splitkv_noalloc(q, k, v, num_splits: int = 0, causal: bool = False, scale: float | None = None,
+                        out=None, lse=None, out_dtype=None, return_lse: bool = True):
+    """fa_fwd_splitkv_noalloc: the decode forward with its split-KV partial
+    results in the library's fixed device scratch (32 MiB per GPU) -- the C
+    call allocates nothing (pass ``out``/``lse`` to keep this function from
+    allocating them).  Calls that overlap on one GPU share the scratch and
+    must be ordered."""
+    from . import _lib
+
+    lib = _lib.load()
+    torch = _torch()
+    (B, Hq, Hkv, Nq, Nk, D), out, lse, odt = _prepare(q, k, v, out, lse, out_dtype, return_lse)
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    codes = _codes()
+    stream = torch.cuda.current_stream(q.device).cuda_stream
+    with torch.cuda.device(q.device):
+        st = lib.fa_fwd_splitkv_noalloc(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                                        lse.data_ptr() if lse is not None else None, B, Hq, Hkv, Nq, Nk,
+                                        D, int(bool(causal)), float(scale), stream, codes[q.dtype],
+                                        codes.get(odt, -1), int(num_splits))
+    _check(lib, st)
+    return out, lse
 
 
 def fwd_splitkv(q, k, v, num_splits: int, **kw):

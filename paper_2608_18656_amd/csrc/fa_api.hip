@@ -99,6 +99,34 @@ struct CallWs {
     size_t bytes;
 };
 
+// Fixed device scratch of fa_fwd_splitkv_noalloc: the split-KV partial results
+// of its calls live here (each GPU holds its own copy until the process
+// ends).  Host code never passes `scratch` itself to a kernel (on the host
+// that name is a stand-in, not a device address): the address of the
+// device's copy is read once per device with hipGetSymbolAddress and kept.
+constexpr size_t kScratchBytes = (size_t)32 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+void *g_scratch_ptr[kMaxDevices];
+std::mutex g_scratch_mu;
+
+// Device address of the current device's scratch (read on the first call per
+// device, with that device current).
+fa_status_t scratch_address(void **out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return FA_ERR_HIP;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) {
+            (void)hipGetLastError();
+            return FA_ERR_HIP;
+        }
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return FA_OK;
+}
+
 // The argument checks of every attention entry point.  kv_rows: rows of
 // Hkv * D elements that k and v each hold (-1: B * Nk, the contiguous layout).
 fa_status_t validate_core(const void *q, const void *k, const void *v, const void *o,
@@ -349,6 +377,28 @@ fa_status_t fa_fwd_ws(const void *q, const void *k, const void *v, void *o, floa
                       fa_dtype_t in_dtype, fa_dtype_t out_dtype, int num_splits, void *workspace,
                       size_t workspace_bytes) {
     const CallWs cws{workspace, workspace_bytes};
+    return run(q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, stream, in_dtype, out_dtype,
+               num_splits, 0, nullptr, Paging(), &cws);
+}
+
+fa_status_t fa_fwd_splitkv_noalloc(const void *q, const void *k, const void *v, void *o, float *lse,
+                                   int B, int Hq, int Hkv, int Nq, int Nk, int D, int causal,
+                                   float scale, void *stream, fa_dtype_t in_dtype,
+                                   fa_dtype_t out_dtype, int num_splits) {
+    // the argument checks of fa_fwd_splitkv, then the size of the partial
+    // results against the scratch, all before any HIP call
+    fa_status_t st = validate_core(q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, in_dtype,
+                                   out_dtype, -1);
+    if (st != FA_OK) return st;
+    if (num_splits < 0 || num_splits > FA_MAX_SPLITS) return FA_ERR_SPLITS;
+    CallWs cws{nullptr, 0};
+    if (fa::decode_supported(Nq, D, in_dtype)) {
+        const int S = num_splits > 0 ? num_splits : fa::decode_default_splits(B, Hq, Hkv, Nk, D);
+        if (fa::decode_workspace_bytes(B, Hq, D, S) > kScratchBytes) return FA_ERR_WORKSPACE;
+        st = scratch_address(&cws.ptr);
+        if (st != FA_OK) return st;
+        cws.bytes = kScratchBytes;
+    }
     return run(q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, stream, in_dtype, out_dtype,
                num_splits, 0, nullptr, Paging(), &cws);
 }

@@ -265,3 +265,17 @@ def test_per_call_workspace_argument_errors_before_any_launch():
 
     assert paged(ws=None) == 1 and paged(ws=W + 2) == 7 and paged(wsb=need - 16) == 10
     assert paged(ws=O) == 8 and paged(bt=None) == 1
+
+
+def test_noalloc_size_limit_before_any_launch():
+    """fa_fwd_splitkv_noalloc refuses partial results beyond its 32 MiB
+    scratch with FA_ERR_WORKSPACE, after the checks of fa_fwd_splitkv, before
+    any HIP call (fake addresses)."""
+    lib = _lib.load()
+    far = [k << 40 for k in range(1, 6)]
+    BF16 = _lib.FA_BF16
+    # 256 * 64 * 16 * (128 + 2) * 4 B = 136 MB of partials
+    assert lib.fa_fwd_splitkv_noalloc(*far, 256, 64, 8, 1, 65536, 128, 0, 0.088, None, BF16, BF16, 16) == 10
+    assert lib.fa_workspace_bytes(256, 64, 8, 1, 65536, 128, BF16, 16) > (32 << 20)
+    assert lib.fa_fwd_splitkv_noalloc(*far, 256, 64, 8, 1, 65536, 128, 0, 0.088, None, BF16, BF16, 300) == 12
+    assert lib.fa_fwd_splitkv_noalloc(None, *far[1:], 2, 8, 2, 1, 100, 64, 0, 0.1, None, BF16, BF16, 0) == 1
