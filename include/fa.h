@@ -61,15 +61,21 @@
 
 #ifdef __cplusplus
 extern "C" {
+/* In C++ the enumerations below get int as their fixed underlying type, so
+ * that any int a C caller passes is a valid value of the type (the library
+ * then rejects unknown codes instead of reading an out-of-range enum). */
+#define FA_ENUM_BASE : int
+#else
+#define FA_ENUM_BASE
 #endif
 
-typedef enum {
+typedef enum FA_ENUM_BASE {
     FA_F16 = 0,  /* IEEE binary16 */
     FA_BF16 = 1, /* bfloat16 */
     FA_F32 = 2   /* IEEE binary32 */
 } fa_dtype_t;
 
-typedef enum {
+typedef enum FA_ENUM_BASE {
     FA_OK = 0,
     FA_ERR_NULL = 1,         /* q, k, v or o is NULL */
     FA_ERR_DIM = 2,          /* a size is < 1, or an index would overflow int64 */
