@@ -135,7 +135,34 @@ def loaded_sclk_mhz(torch, call, seconds=2.0):
     return round(sum(clocks) / len(clocks), 1) if clocks else None
 
 
-def run_workload(torch, fa, w, steps, warmup, kv_sets=1, num_splits=None, packing=None):
+# Workgroup layouts of the packing ablation: (label, query slots per
+# workgroup, query heads among them).  Every staged K/V tile serves all slots
+# of its workgroup: one slot (no sharing), four row blocks of one head, four
+# heads of one K/V group (the default), eight heads of an MQA group.
+LAYOUTS = {
+    "gqa_prefill_bf16": [("unshared", 1, 1), ("per_head", 4, 1), ("packed", 4, 4)],
+    "gqa_prefill_d128_f16": [("unshared", 1, 1), ("per_head", 4, 1), ("packed", 4, 4)],
+    "mqa_prefill_f16": [("unshared", 1, 1), ("packed", 4, 4), ("packed_wide", 8, 8)],
+}
+
+
+def staged_kv_bytes(w, slots: int, heads: int) -> int:
+    """K and V bytes the workgroups of one prefill launch copy into LDS with
+    this layout: each workgroup (slots / heads row blocks of 32 rows, heads
+    query heads of one K/V head) stages every tile of keys its causal extent
+    reaches once, K and V (tiles of 64 keys at D = 64, 32 at D = 128)."""
+    bc = 64 if w.D == 64 else 32
+    rows = 32 * (slots // heads)
+    tiles = 0
+    for mb in range((w.Nq + rows - 1) // rows):
+        last = min((mb + 1) * rows, w.Nq) - 1
+        kend = min(w.Nk, last + w.Nk - w.Nq + 1) if w.causal else w.Nk
+        tiles += (kend + bc - 1) // bc
+    groups = w.B * w.Hkv * ((w.Hq // w.Hkv) // heads)
+    return tiles * groups * bc * w.D * 2 * 2
+
+
+def run_workload(torch, fa, w, steps, warmup, kv_sets=1, num_splits=None, packing=None, slots=None):
     from paper_2608_18656_amd.inputs import make_workload
 
     q, k, v = make_workload(w)
@@ -150,7 +177,8 @@ def run_workload(torch, fa, w, steps, warmup, kv_sets=1, num_splits=None, packin
     def make(i):
         qd, kd, vd = sets[i]
         return lambda: fa.fwd(qd, kd, vd, causal=w.causal, scale=w.softmax_scale, out=outs[i],
-                              lse=lses[i], num_splits=num_splits, heads_per_workgroup=packing)
+                              lse=lses[i], num_splits=num_splits, heads_per_workgroup=packing,
+                              slots_per_workgroup=slots)
 
     ms = time_calls(torch, [make(i) for i in range(len(sets))], steps, warmup)
     return ms, sets[0], outs[0], lses[0]
@@ -470,7 +498,8 @@ def q8_decode_step(torch, fa, steps, warmup, with_cpu):
     return out
 
 
-def profile_only(torch, fa, what: str, reps: int, copy_bytes: int, page_size: int):
+def profile_only(torch, fa, what: str, reps: int, copy_bytes: int, page_size: int,
+                 slots: int | None = None, heads: int | None = None):
     """A minimal run for a profiler (rocprofv3 kernel traces and counters):
     ``reps`` calls of one thing and nothing else.  ``what`` is a workload name
     (the attention forward on it), ``copy`` (a plain device copy of
@@ -479,7 +508,8 @@ def profile_only(torch, fa, what: str, reps: int, copy_bytes: int, page_size: in
     x), ``paged_<workload>`` (decode against its K/V in shuffled pages of
     ``page_size`` keys), ``unfused_<workload>`` (the unfused path) or
     ``chunked_prefill`` (the benchmark's chunked prefill, contiguous cache then
-    paged).  Returns a description of what ran."""
+    paged).  ``slots`` and ``heads`` set a prefill workload's workgroup layout
+    (fa_fwd_slots).  Returns a description of what ran."""
     from paper_2608_18656_amd.inputs import Q8_LAYER_SHAPES, WORKLOADS, make_q8_0, make_qkv, make_workload
 
     def done(desc):
@@ -542,8 +572,10 @@ def profile_only(torch, fa, what: str, reps: int, copy_bytes: int, page_size: in
     w = WORKLOADS[what]
     q, k, v = (t.cuda() for t in make_workload(w))
     for _ in range(reps):
-        fa.fwd(q, k, v, causal=w.causal, scale=w.softmax_scale)
-    return done(f"attention forward on {w.name}")
+        fa.fwd(q, k, v, causal=w.causal, scale=w.softmax_scale, slots_per_workgroup=slots,
+               heads_per_workgroup=heads)
+    return done(f"attention forward on {w.name}" +
+                (f" ({slots} slots, {heads} heads per workgroup)" if slots else ""))
 
 
 def main():
@@ -565,6 +597,8 @@ def main():
     ap.add_argument("--reps", type=int, default=5, help="calls for --only")
     ap.add_argument("--copy-bytes", type=int, default=1 << 28, help="bytes of the --only copy run")
     ap.add_argument("--page-size", type=int, default=256, help="page size of the --only paged run")
+    ap.add_argument("--slots", type=int, default=None, help="--only prefill run: query slots per workgroup")
+    ap.add_argument("--heads", type=int, default=None, help="--only prefill run: query heads per workgroup")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -583,8 +617,8 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     if args.only:
-        print(json.dumps(profile_only(torch, fa, args.only, args.reps, args.copy_bytes, args.page_size)),
-              flush=True)
+        print(json.dumps(profile_only(torch, fa, args.only, args.reps, args.copy_bytes, args.page_size,
+                                      args.slots, args.heads)), flush=True)
         return
     w = WORKLOADS[args.workload]
     decode_main = w.Nq == 1
@@ -664,23 +698,29 @@ def main():
                                  "algorithmic_per_launch": x.kv_bytes()}}
             log(f"[bench] {name}: {xms * 1e3:.1f} us/call, {val:.1f} {u} ({100 * val / pk:.1f}%)")
             torch.cuda.empty_cache()
-        # inter-head packing ablation: the default schedule (the G query heads
-        # of a K/V group share each staged K/V tile) against the per-head one
+        # inter-head packing ablation: workgroup layouts that differ in how many
+        # query slots (heads or row blocks) each staged K/V tile serves
         ablation = []
-        for name in (() if args.no_ablation else
-                     ("gqa_prefill_bf16", "gqa_prefill_d128_f16", "mqa_prefill_f16")):
+        for name in (() if args.no_ablation else tuple(LAYOUTS)):
             x = WORKLOADS[name]
             steps = max(5, min(args.steps, 20))
-            row = {"workload": name}
-            for label, hw in (("packed", None), ("per_head", 1)):
-                xms, *_ = run_workload(torch, fa, x, steps, 3, packing=hw)
-                row[label + "_us"] = round(xms * 1e3, 2)
-                row[label + "_tflops"] = round(x.flops() / (xms * 1e-3) / 1e12, 1)
+            row = {"workload": name, "layouts": []}
+            for label, ns, hw in LAYOUTS[name]:
+                xms, *_ = run_workload(torch, fa, x, steps, 3, packing=hw, slots=ns)
+                row["layouts"].append({
+                    "layout": label, "slots_per_workgroup": ns, "heads_per_workgroup": hw,
+                    "us": round(xms * 1e3, 2), "tflops": round(x.flops() / (xms * 1e-3) / 1e12, 1),
+                    "staged_kv_bytes": staged_kv_bytes(x, ns, hw),
+                    "hbm_fetch_bytes": stored_traffic("prefill_kernel", f"{name}_slots{ns}_heads{hw}",
+                                                      PREFILL_SOURCES)})
                 torch.cuda.empty_cache()
-            row["speedup"] = round(row["per_head_us"] / row["packed_us"], 3)
+            base = row["layouts"][0]["us"]
+            for lay in row["layouts"]:
+                lay["speedup_vs_unshared"] = round(base / lay["us"], 3)
             ablation.append(row)
-            log(f"[bench] packing {name}: packed {row['packed_us']} us, per-head "
-                f"{row['per_head_us']} us ({row['speedup']}x)")
+            log(f"[bench] packing {name}: " + ", ".join(
+                f"{lay['layout']} {lay['us']} us ({lay['staged_kv_bytes'] / 1e6:.0f} MB staged)"
+                for lay in row["layouts"]))
         if ablation:
             result["packing_ablation"] = ablation
         # fused against unfused self-attention (score matrix S in fp32 and

@@ -89,7 +89,7 @@ typedef enum FA_ENUM_BASE {
     FA_ERR_WORKSPACE = 10,   /* workspace allocation failed or not allowed (stream capture), or a caller-owned one is too small */
     FA_ERR_HIP = 11,         /* a HIP runtime call or kernel launch failed */
     FA_ERR_SPLITS = 12,      /* num_splits outside [0, FA_MAX_SPLITS] */
-    FA_ERR_PACKING = 13      /* heads_per_workgroup not 0, 1, 2 or 4, or not a divisor of Hq / Hkv */
+    FA_ERR_PACKING = 13      /* slots or heads per workgroup not allowed (see fa_fwd_slots) */
 } fa_status_t;
 
 #define FA_MAX_SPLITS 256
@@ -144,11 +144,30 @@ fa_status_t fa_fwd_splitkv(const void *q, const void *k, const void *v, void *o,
  * is the same, bit for bit, for every packing.  Only the fp16 / bf16 prefill
  * kernels (Nq > 1, D in {64, 128}) take the packing; other calls ignore it.
  * Errors: FA_ERR_PACKING for a value other than 0, 1, 2, 4 or one that does
- * not divide Hq / Hkv; otherwise as fa_fwd. */
+ * not divide Hq / Hkv; otherwise as fa_fwd.  (fa_fwd_slots also sets the
+ * number of slots.) */
 fa_status_t fa_fwd_packed(const void *q, const void *k, const void *v, void *o, float *lse,
                           int B, int Hq, int Hkv, int Nq, int Nk, int D, int causal,
                           float scale, void *stream, fa_dtype_t in_dtype,
                           fa_dtype_t out_dtype, int heads_per_workgroup);
+
+/* Prefill with an explicit workgroup layout, for the packing ablation: each
+ * prefill workgroup holds slots_per_workgroup query slots of 32 rows that all
+ * read one key/value head, so every K/V tile it stages in LDS serves that many
+ * slots (the reuse the inter-head packing of Sec. 4.1.1 and Fig. 1 is about:
+ * one load of a key/value row serving several query heads), and
+ * heads_per_workgroup of them are different query heads of the group (the
+ * rest consecutive row blocks).  slots_per_workgroup: 0 (the default, 4), 1
+ * (no sharing: every slot stages its own tiles), 2, 4 or 8;
+ * heads_per_workgroup: 0 (the most heads, up to 4, that divide both the slots
+ * and Hq / Hkv), 1, 2, 4 or 8, dividing Hq / Hkv and the slots.  The result
+ * is the same, bit for bit, for every layout.  Only the fp16 / bf16 prefill
+ * kernels (Nq > 1, D in {64, 128}) take the layout; other calls ignore it.
+ * Errors: FA_ERR_PACKING for a value not allowed; otherwise as fa_fwd. */
+fa_status_t fa_fwd_slots(const void *q, const void *k, const void *v, void *o, float *lse, int B,
+                         int Hq, int Hkv, int Nq, int Nk, int D, int causal, float scale, void *stream,
+                         fa_dtype_t in_dtype, fa_dtype_t out_dtype, int slots_per_workgroup,
+                         int heads_per_workgroup);
 
 /* Attention against a key/value cache with per-sequence lengths (decode,
  * and chunked prefill of Nq new tokens).  k and v are [B][Nk][Hkv][D]

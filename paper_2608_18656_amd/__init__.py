@@ -80,7 +80,7 @@ def _workspace_arg(workspace, device):
 
 def fwd(q, k, v, causal: bool = False, scale: float | None = None, out=None, lse=None,
         out_dtype=None, return_lse: bool = True, num_splits: int | None = None,
-        heads_per_workgroup: int | None = None, workspace=None):
+        heads_per_workgroup: int | None = None, workspace=None, slots_per_workgroup: int | None = None):
     """Attention forward o = softmax(scale * q k^T) v on the GPU.
 
     q [B, Nq, Hq, D], k and v [B, Nk, Hkv, D] (contiguous, same dtype and
@@ -90,7 +90,8 @@ def fwd(q, k, v, causal: bool = False, scale: float | None = None, out=None, lse
     ``out_dtype=torch.float32`` returns the kernel's fp32 result before the
     final rounding.  ``num_splits`` forces the decode split count (decode
     shapes only); ``heads_per_workgroup`` (1, 2 or 4) forces the prefill
-    query-head packing (see fa_fwd_packed).  ``workspace`` (a contiguous uint8
+    query-head packing (see fa_fwd_packed) and ``slots_per_workgroup`` (1, 2, 4
+    or 8) the prefill workgroup layout (fa_fwd_slots).  ``workspace`` (a contiguous uint8
     GPU tensor of at least workspace_bytes(...) bytes) is this call's own
     decode workspace (fa_fwd_ws); otherwise the library-owned one of the
     current stream is used.  Returns (out, lse) with lse
@@ -110,9 +111,14 @@ def fwd(q, k, v, causal: bool = False, scale: float | None = None, out=None, lse
             lse.data_ptr() if lse is not None else None, B, Hq, Hkv, Nq, Nk, D,
             int(bool(causal)), float(scale), stream, codes[q.dtype], codes.get(odt, -1))
     with torch.cuda.device(q.device):
-        if heads_per_workgroup is not None and (num_splits is not None or workspace is not None):
+        if (heads_per_workgroup is not None and slots_per_workgroup is None
+                and (num_splits is not None or workspace is not None)):
             raise ValueError("heads_per_workgroup excludes num_splits and workspace")
-        if workspace is not None:
+        if slots_per_workgroup is not None:
+            if num_splits is not None or workspace is not None:
+                raise ValueError("slots_per_workgroup excludes num_splits and workspace")
+            st = lib.fa_fwd_slots(*args, int(slots_per_workgroup), int(heads_per_workgroup or 0))
+        elif workspace is not None:
             st = lib.fa_fwd_ws(*args, int(num_splits or 0), *_workspace_arg(workspace, q.device))
         elif num_splits is not None:
             st = lib.fa_fwd_splitkv(*args, int(num_splits))

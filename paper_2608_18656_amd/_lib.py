@@ -27,7 +27,7 @@ EXPORTS = ("fa_status_string", "fa_version", "fa_validate", "fa_fwd_f16", "fa_fw
            "fa_fwd_f32", "fa_fwd", "fa_fwd_splitkv", "fa_workspace_bytes",
            "fa_release_workspace", "fa_set_workspace", "fa_fwd_packed", "fa_fwd_kvcache",
            "fa_q8_0_gemv", "fa_fwd_kvcache_paged", "fa_fwd_unfused", "fa_unfused_workspace_bytes",
-           "fa_fwd_ws", "fa_fwd_kvcache_ws", "fa_fwd_kvcache_paged_ws", "fa_fwd_splitkv_noalloc")
+           "fa_fwd_ws", "fa_fwd_kvcache_ws", "fa_fwd_kvcache_paged_ws", "fa_fwd_splitkv_noalloc", "fa_fwd_slots")
 
 _lib = None
 
@@ -63,6 +63,8 @@ def load():
     lib.fa_fwd_splitkv.restype = _I
     lib.fa_fwd_packed.argtypes = [_P, _P, _P, _P, _P] + _DIMS + [_P, _I, _I, _I]
     lib.fa_fwd_packed.restype = _I
+    lib.fa_fwd_slots.argtypes = [_P, _P, _P, _P, _P] + _DIMS + [_P, _I, _I, _I, _I]
+    lib.fa_fwd_slots.restype = _I
     lib.fa_fwd_kvcache.argtypes = [_P, _P, _P, _P, _P, _P] + _DIMS + [_P, _I, _I]
     lib.fa_fwd_kvcache.restype = _I
     lib.fa_workspace_bytes.argtypes = [_I] * 6 + [_I, _I]

@@ -128,15 +128,17 @@ fa_status_t run(const void *q, const void *k, const void *v, void *o, float *lse
                 int Hkv, int Nq, int Nk, int D, int causal, float scale, void *stream,
                 fa_dtype_t in, fa_dtype_t out, int splits_req, int hw_req = 0,
                 const int *seqlens = nullptr, const Paging &pg = Paging(),
-                const CallWs *cws = nullptr) {
+                const CallWs *cws = nullptr, int slots_req = 0) {
     const long long kv_rows = pg.block_table ? (long long)pg.num_pages * pg.page_size : -1;
     fa_status_t st = validate_core(q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, in, out, kv_rows);
     if (st != FA_OK) return st;
     if (splits_req < 0 || splits_req > FA_MAX_SPLITS) return FA_ERR_SPLITS;
-    if (!(hw_req == 0 || hw_req == 1 || hw_req == 2 || hw_req == 4) ||
-        (hw_req > 0 && (Hq / Hkv) % hw_req != 0))
+    const int slots = slots_req > 0 ? slots_req : 4;
+    if (!(slots_req == 0 || slots_req == 1 || slots_req == 2 || slots_req == 4 || slots_req == 8) ||
+        !(hw_req == 0 || hw_req == 1 || hw_req == 2 || hw_req == 4 || hw_req == 8) ||
+        (hw_req > 0 && ((Hq / Hkv) % hw_req != 0 || slots % hw_req != 0)))
         return FA_ERR_PACKING;
-    fa::Problem p{q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, in, out, hw_req, seqlens,
+    fa::Problem p{q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, in, out, hw_req, slots_req, seqlens,
                   pg.block_table, pg.page_size, pg.max_pages, pg.num_pages};
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     hipError_t e;
@@ -193,7 +195,8 @@ const char *fa_status_string(fa_status_t s) {
     case FA_ERR_HIP: return "FA_ERR_HIP: HIP runtime or launch error";
     case FA_ERR_SPLITS: return "FA_ERR_SPLITS: num_splits out of range";
     case FA_ERR_PACKING:
-        return "FA_ERR_PACKING: heads_per_workgroup must be 0, 1, 2 or 4 and divide Hq / Hkv";
+        return "FA_ERR_PACKING: slots_per_workgroup must be 0, 1, 2, 4 or 8; heads_per_workgroup 0, 1, 2, 4 or "
+               "8, dividing Hq / Hkv and the slots";
     }
     return "unknown fa_status_t";
 }
@@ -311,6 +314,14 @@ fa_status_t kvcache_paged(const void *q, const void *k_pages, const void *v_page
 }  // namespace
 
 extern "C" {
+
+fa_status_t fa_fwd_slots(const void *q, const void *k, const void *v, void *o, float *lse, int B,
+                         int Hq, int Hkv, int Nq, int Nk, int D, int causal, float scale, void *stream,
+                         fa_dtype_t in_dtype, fa_dtype_t out_dtype, int slots_per_workgroup,
+                         int heads_per_workgroup) {
+    return run(q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, stream, in_dtype, out_dtype, 0,
+               heads_per_workgroup, nullptr, Paging(), nullptr, slots_per_workgroup);
+}
 
 fa_status_t fa_fwd_kvcache(const void *q, const void *k, const void *v, void *o, float *lse,
                            const int *seqlens_k, int B, int Hq, int Hkv, int Nq, int Nk, int D,
@@ -446,7 +457,7 @@ fa_status_t fa_fwd_unfused(const void *q, const void *k, const void *v, void *o,
         overlaps(workspace, need, v, kb) || overlaps(workspace, need, o, ob) ||
         (lse && overlaps(workspace, need, lse, lb)))
         return FA_ERR_ALIAS;
-    fa::Problem p{q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, in_dtype, out_dtype, 0,
+    fa::Problem p{q, k, v, o, lse, B, Hq, Hkv, Nq, Nk, D, causal, scale, in_dtype, out_dtype, 0, 0,
                   nullptr, nullptr, 0, 0, 0};
     const hipError_t e = fa::launch_unfused(p, workspace, reinterpret_cast<hipStream_t>(stream));
     return e == hipSuccess ? FA_OK : FA_ERR_HIP;

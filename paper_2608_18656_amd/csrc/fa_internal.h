@@ -18,6 +18,7 @@ struct Problem {
     float scale;
     fa_dtype_t in, out;
     int hw;   // prefill query heads per workgroup (0: the default choice)
+    int slots;   // prefill 32-row query slots per workgroup (0: the default, 4)
     const int *seqlens;   // device [B]: valid keys per batch element (NULL: Nk for all)
     // Paged K/V (block_table != NULL): k and v are [num_pages][page_size][Hkv][D];
     // key j of batch element b is row j % page_size of page

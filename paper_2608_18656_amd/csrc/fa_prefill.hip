@@ -48,7 +48,7 @@ namespace fa {
 namespace {
 
 constexpr int WR = 32;        // query rows per slot
-constexpr int NSLOT = 4;      // slots per workgroup
+constexpr int NSLOT = 4;      // slots per workgroup (the default; 1, 2 and 8 also exist)
 constexpr float kMaxLaneSum = 4096.0f;   // largest 16-weight lane sum kept without a rescale
 
 struct PrefillArgs {
@@ -58,8 +58,8 @@ struct PrefillArgs {
     int B, Hq, Hkv, Nq, Nk;
     float c;          // max(|scale|, tiny) * log2(e), > 0
     unsigned qsign;   // 0x80008000 to negate q (scale < 0), else 0
-    int HW;           // query heads per workgroup (1, 2 or 4)
-    int nmb;          // row blocks of 32 * (4 / HW) rows
+    int HW;           // query heads per workgroup (1, 2, 4 or 8)
+    int nmb;          // row blocks of 32 * (slots / HW) rows
     int nhg;          // head groups per key/value head (G / HW)
     int pair;         // 1: every workgroup is resident at once; order heavy/light pairs
     const int *seqlens;   // valid keys per batch element (NULL: Nk for all)
@@ -74,27 +74,46 @@ struct PrefillArgs {
 // that, so one wave per slot (32-key tiles) and 4-wave workgroups, three per
 // CU (three waves per SIMD, from independent workgroups; operands are read
 // from LDS in small groups to fit 168 VGPRs).  Two LDS stages in both.
-template <int D> struct Cfg {
+// NS, the slots per workgroup (all reading one key/value head, each staged
+// tile serving all of them), is 4 by default; 1, 2 and 8 exist for the
+// packing ablation (fewer slots stage more per thread, so they hold fewer
+// waves per SIMD).
+template <int D, int NS = NSLOT> struct Cfg {
     static constexpr int NQ = D == 64 ? 2 : 1;       // waves per slot
-    static constexpr int WPE = D == 64 ? 4 : 3;      // waves per SIMD
-    static constexpr int WPC = D == 64 ? 2 : 3;      // workgroups per CU
+    static constexpr int WPE = D == 64 ? (NS >= 4 ? 4 : 3) : (NS >= 4 ? 3 : 2);   // waves per SIMD
+    static constexpr int NWG = NS * NQ;              // waves per workgroup
+    static constexpr int WPC = NWG >= 4 * WPE ? 1 : 4 * WPE / NWG;   // workgroups per CU (registers)
     static constexpr int BC = 32 * NQ;               // keys per tile
-    static constexpr int NT = 64 * NSLOT * NQ;       // threads per workgroup
+    static constexpr int NT = 64 * NWG;              // threads per workgroup
     static constexpr int NSTAGE = 2;                 // LDS tile stages
     static constexpr int KS = D + 8;                 // K row stride in 16-bit elements
     static constexpr int VTS = BC + 8;               // V^T row stride: BC key positions + pad
     static constexpr int KSZ = BC * KS;
     static constexpr int VSZ = D * VTS;
     static constexpr int STAGE = KSZ + VSZ;
-    static constexpr int MERGE = NQ > 1 ? NSLOT * (NQ / 2) * ((D / 32) * 16 + 2) * 64 : 0;  // floats
+    static constexpr int MERGE = NQ > 1 ? NS * (NQ / 2) * ((D / 32) * 16 + 2) * 64 : 0;  // floats
     static constexpr int WORDS = (NSTAGE * STAGE) > (2 * MERGE) ? NSTAGE * STAGE : 2 * MERGE;
+    // Staging split.  KCH 16-byte K chunks and VUN V key-pair units (two
+    // 16-byte loads each) per tile.  With two or more waves the upper half of
+    // the workgroup stages K and the lower half V (SH threads each); a
+    // one-wave workgroup stages both itself.
+    static constexpr int KCH = BC * (D / 8);
+    static constexpr int VUN = (BC / 2) * (D / 8);
+    static constexpr bool BOTH = NT < 128;
+    static constexpr int SH = BOTH ? NT : NT / 2;
+    static constexpr int KPT = KCH / SH;                      // K chunks per staging thread
+    static constexpr int VPT = VUN >= SH ? VUN / SH : 1;      // V units per staging thread
+    static constexpr bool VPART = VUN < SH;                   // only the first VUN V threads stage
+    static constexpr int SL = BOTH ? KPT + 2 * VPT : (KPT > 2 * VPT ? KPT : 2 * VPT);   // loads in flight
+    static_assert(KCH % SH == 0 && (VUN % SH == 0 || SH % VUN == 0), "staging split");
 };
 
-template <typename TIN, typename TOUT, int D, bool CAUSAL, bool PAGED>
-__global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<D>::WPE, Cfg<D>::WPE))) void prefill_kernel(PrefillArgs a) {
+template <typename TIN, typename TOUT, int D, int NS, bool CAUSAL, bool PAGED>
+__global__ __launch_bounds__((Cfg<D, NS>::NT)) __attribute__((amdgpu_waves_per_eu((Cfg<D, NS>::WPE), (Cfg<D, NS>::WPE)))) void prefill_kernel(PrefillArgs a) {
     using S = typename TIN::scalar;
     using V8 = typename TIN::vec8;
-    using SM = Cfg<D>;
+    using SM = Cfg<D, NS>;
+    constexpr int NSLOT = NS;
     constexpr int NQ = SM::NQ, BC = SM::BC, NT = SM::NT, NSTAGE = SM::NSTAGE;
     constexpr int KSTEPS = D / 16;          // QK^T contraction steps
     constexpr int DT = D / 32;              // output column tiles
@@ -158,30 +177,45 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
     }
 
     // Tile staging.  The second half of the workgroup copies K rows (chunk
-    // c = st + (NT / 2) i: key c / CPR, 16-byte column chunk c % CPR); the first
+    // c = st + SH i: key c / CPR, 16-byte column chunk c % CPR); the first
     // half stages V transposed: unit u holds keys 2p, 2p+1 (p = u % KP) of
     // column chunk u / KP and writes eight 32-bit words, each the (2p, 2p+1)
     // pair of one column d, into row d of V^T (as fp16).  Within every 16 keys
     // the V^T positions swap bits 2 and 3 of the key index, so that the eight
-    // keys one MFMA lane needs are contiguous.  Loads are buffer loads: the
-    // tile's first key row is the (scalar) base and each lane keeps a fixed
-    // byte offset, so a step spends no vector instructions on addresses.
-    constexpr int SL = BC * D / (4 * NT);       // 16-byte loads per thread per tile
+    // keys one MFMA lane needs are contiguous.  (A one-wave workgroup stages
+    // both: its loads 0 .. KPT-1 are K chunks, the rest V units.)  Loads are
+    // buffer loads: the tile's first key row is the (scalar) base and each
+    // lane keeps a fixed byte offset, so a step spends no vector instructions
+    // on addresses.
+    constexpr int SL = SM::SL;                  // 16-byte loads in flight per thread
+    constexpr int KPT = SM::KPT, VPT = SM::VPT, SH = SM::SH;
+    constexpr bool BOTH = SM::BOTH;
     constexpr int KP = BC / 2;                  // key pairs per tile
+    static_assert(!(BOTH && PAGED), "paged K/V takes the default slots");
     // second half of the workgroup: K (wave-uniform).  The older wave of each
     // SIMD wins issue priority and finishes its softmax first, so it takes the
     // heavier V staging (the bf16 conversion) and the later one the K copy.
-    const bool kgroup = w >= NT / 128;
-    const S *kvbase = reinterpret_cast<const S *>(kgroup ? a.k : a.v) +
+    const bool kgroup = !BOTH && w >= NT / 128;
+    // the tensor this thread's loads read: K for the K half (and for the
+    // K loads of a one-wave workgroup, whose V loads use vnext below)
+    const S *kvbase = reinterpret_cast<const S *>((kgroup || BOTH) ? a.k : a.v) +
                       ((size_t)b * a.Nk * a.Hkv + g) * D;
     const int st = kgroup ? tid - NT / 2 : tid;
+    // loads this thread issues per tile (wave-uniform; FULL: SL for every thread)
+    constexpr bool FULL = !BOTH && KPT == 2 * VPT && !SM::VPART;
+    const int nload = BOTH ? SL : kgroup ? KPT : (SM::VPART && st >= SM::VUN ? 0 : 2 * VPT);
     const size_t row_elems = (size_t)a.Hkv * D;      // elements between consecutive keys
+    auto isk = [&](int i) __attribute__((always_inline)) { return BOTH ? i < KPT : kgroup; };
     // tile-relative key and column of load i of this thread
-    auto lkey = [&](int i) {
-        return kgroup ? (st + (NT / 2) * i) / CPR : 2 * ((st + (NT / 2) * (i >> 1)) % KP) + (i & 1);
+    auto lkey = [&](int i) __attribute__((always_inline)) {
+        if (isk(i)) return (st + SH * i) / CPR;
+        const int j = BOTH ? i - KPT : i;
+        return 2 * ((st + SH * (j >> 1)) % KP) + (j & 1);
     };
-    auto lcol = [&](int i) {
-        return kgroup ? 8 * ((st + (NT / 2) * i) % CPR) : 8 * ((st + (NT / 2) * (i >> 1)) / KP);
+    auto lcol = [&](int i) __attribute__((always_inline)) {
+        if (isk(i)) return 8 * ((st + SH * i) % CPR);
+        const int j = BOTH ? i - KPT : i;
+        return 8 * ((st + SH * (j >> 1)) / KP);
     };
     int goff[SL];                                    // tile-relative byte offsets
 #pragma unroll
@@ -191,6 +225,8 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
     // from there to the end of the last key row (the buffer view, so that
     // keys past the end read as zero); both advance by one tile per load.
     const S *tnext = kvbase;
+    // a one-wave workgroup: the first key row of the next V tile
+    const S *vnext = reinterpret_cast<const S *>(a.v) + ((size_t)b * a.Nk * a.Hkv + g) * D;
     long long rem = (long long)(Nk - 1) * (long long)row_elems * (long long)sizeof(S) +
                     (long long)D * (long long)sizeof(S);
     // paged K/V: the pool of pages, at head g.  Tiles are loaded in order
@@ -213,7 +249,7 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
         tcur = __builtin_amdgcn_raw_buffer_load_b32(trs, 0, 0, 0);
         tnx = __builtin_amdgcn_raw_buffer_load_b32(trs, 4, 0, 0);
     }
-    auto gload = [&](int kt) {   // the next tile (tiles are loaded in order; the argument is its first key)
+    auto gload = [&](int kt) __attribute__((always_inline)) {   // the next tile (tiles are loaded in order; the argument is its first key)
         int nrec;
         if constexpr (PAGED) {
             // the tile's rows sit in one page (pages hold a multiple of 64
@@ -238,9 +274,19 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
         }
         const __amdgpu_buffer_rsrc_t rs =
             __builtin_amdgcn_make_buffer_rsrc(const_cast<S *>(tnext), (short)0, nrec, 0x00020000);
+        if constexpr (BOTH) {
+            const __amdgpu_buffer_rsrc_t rv =
+                __builtin_amdgcn_make_buffer_rsrc(const_cast<S *>(vnext), (short)0, nrec, 0x00020000);
 #pragma unroll
-        for (int i = 0; i < SL; ++i)
-            sr[i] = __builtin_bit_cast(uint4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, goff[i], 0, 0));
+            for (int i = 0; i < SL; ++i)
+                sr[i] = __builtin_bit_cast(uint4_t, __builtin_amdgcn_raw_buffer_load_b128(i < KPT ? rs : rv, goff[i], 0, 0));
+            vnext += (size_t)BC * row_elems;
+        } else {
+#pragma unroll
+            for (int i = 0; i < SL; ++i)
+                if (FULL || i < nload)
+                    sr[i] = __builtin_bit_cast(uint4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, goff[i], 0, 0));
+        }
         if constexpr (!PAGED) {
             tnext += (size_t)BC * row_elems;
             rem -= (long long)BC * (long long)row_elems * (long long)sizeof(S);
@@ -255,36 +301,42 @@ __global__ __launch_bounds__(Cfg<D>::NT) __attribute__((amdgpu_waves_per_eu(Cfg<
         }
     };
     // LDS destination (element offset inside a stage) of load i
-    auto sdst = [&](int i) {
-        if (kgroup) return lkey(i) * SM::KS + lcol(i);
+    auto sdst = [&](int i) __attribute__((always_inline)) {
+        if (isk(i)) return lkey(i) * SM::KS + lcol(i);
         const int key = lkey(i) & ~1;
         const int pos = (key & ~12) | ((key & 4) << 1) | ((key & 8) >> 1);
         return SM::KSZ + lcol(i) * SM::VTS + pos;   // row d = lcol + e, position pos
     };
-    auto sstore = [&](unsigned short *stage) {
-        if (kgroup) {
+    auto sstore_v = [&](unsigned short *stage, int i0) __attribute__((always_inline)) {   // the V unit of loads i0, i0 + 1
+        unsigned *vt = reinterpret_cast<unsigned *>(stage + sdst(i0));
+        const uint4_t x = sr[i0], y = sr[i0 + 1];
 #pragma unroll
-            for (int i = 0; i < SL; ++i) st16(stage + sdst(i), sr[i]);
-        } else {
-#pragma unroll
-            for (int u = 0; u < SL / 2; ++u) {
-                unsigned *vt = reinterpret_cast<unsigned *>(stage + sdst(2 * u));
-                const uint4_t x = sr[2 * u], y = sr[2 * u + 1];
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const unsigned xe = x[e >> 1], ye = y[e >> 1];
-                    unsigned w;
-                    if constexpr (IN_BF16) {
-                        const float fx = __uint_as_float((e & 1) ? (xe & 0xffff0000u) : (xe << 16));
-                        const float fy = __uint_as_float((e & 1) ? (ye & 0xffff0000u) : (ye << 16));
-                        w = pack_f16x2(fx, fy);
-                    } else {
-                        w = (e & 1) ? __builtin_amdgcn_perm(ye, xe, 0x07060302u)
-                                    : __builtin_amdgcn_perm(ye, xe, 0x05040100u);
-                    }
-                    vt[e * (SM::VTS / 2)] = w;
-                }
+        for (int e = 0; e < 8; ++e) {
+            const unsigned xe = x[e >> 1], ye = y[e >> 1];
+            unsigned w;
+            if constexpr (IN_BF16) {
+                const float fx = __uint_as_float((e & 1) ? (xe & 0xffff0000u) : (xe << 16));
+                const float fy = __uint_as_float((e & 1) ? (ye & 0xffff0000u) : (ye << 16));
+                w = pack_f16x2(fx, fy);
+            } else {
+                w = (e & 1) ? __builtin_amdgcn_perm(ye, xe, 0x07060302u)
+                            : __builtin_amdgcn_perm(ye, xe, 0x05040100u);
             }
+            vt[e * (SM::VTS / 2)] = w;
+        }
+    };
+    auto sstore = [&](unsigned short *stage) __attribute__((always_inline)) {
+        if constexpr (BOTH) {
+#pragma unroll
+            for (int i = 0; i < KPT; ++i) st16(stage + sdst(i), sr[i]);
+#pragma unroll
+            for (int u = 0; u < VPT; ++u) sstore_v(stage, KPT + 2 * u);
+        } else if (kgroup) {
+#pragma unroll
+            for (int i = 0; i < KPT; ++i) st16(stage + sdst(i), sr[i]);
+        } else if (FULL || nload > 0) {
+#pragma unroll
+            for (int u = 0; u < VPT; ++u) sstore_v(stage, 2 * u);
         }
     };
 
@@ -564,8 +616,9 @@ int cu_count() {
     return n;
 }
 
-template <typename TIN, typename TOUT, int D, bool CAUSAL>
+template <typename TIN, typename TOUT, int D, int NS, bool CAUSAL>
 hipError_t launch_t(const Problem &p, hipStream_t stream) {
+    using SM = Cfg<D, NS>;
     PrefillArgs a;
     a.q = p.q; a.k = p.k; a.v = p.v; a.o = p.o; a.lse = p.lse;
     a.B = p.B; a.Hq = p.Hq; a.Hkv = p.Hkv; a.Nq = p.Nq; a.Nk = p.Nk;
@@ -579,29 +632,49 @@ hipError_t launch_t(const Problem &p, hipStream_t stream) {
     a.c = __builtin_fmaxf(__builtin_fabsf(p.scale), 1e-30f) * kLog2e;
     a.qsign = p.scale < 0.f ? 0x80008000u : 0u;
     const int G = p.Hq / p.Hkv;
-    a.HW = p.hw > 0 ? p.hw : ((NSLOT % 4 == 0 && G % 4 == 0) ? 4 : (G % 2 == 0 ? 2 : 1));
-    const int RB = NSLOT / a.HW;
+    // query heads per workgroup: the requested packing, else the most heads
+    // of one key/value group (up to 4) that fill the slots evenly
+    int hw = 1;
+    for (int c = 2; c <= (NS < 4 ? NS : 4); c *= 2)
+        if (NS % c == 0 && G % c == 0) hw = c;
+    a.HW = p.hw > 0 ? p.hw : hw;
+    const int RB = NS / a.HW;
     a.nmb = (p.Nq + WR * RB - 1) / (WR * RB);
     a.nhg = G / a.HW;
     a.pair = 0;
     const long long nblocks = (long long)a.nmb * p.B * p.Hkv * a.nhg;
     if (nblocks <= 0) return hipSuccess;
     if (nblocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-    if (p.causal) a.pair = nblocks <= (long long)Cfg<D>::WPC * cu_count() ? 1 : 0;
-    if (p.block_table)
-        hipLaunchKernelGGL((prefill_kernel<TIN, TOUT, D, CAUSAL, true>), dim3((unsigned)nblocks),
-                           dim3(Cfg<D>::NT), 0, stream, a);
-    else
-        hipLaunchKernelGGL((prefill_kernel<TIN, TOUT, D, CAUSAL, false>), dim3((unsigned)nblocks),
-                           dim3(Cfg<D>::NT), 0, stream, a);
+    if (p.causal) a.pair = nblocks <= (long long)SM::WPC * cu_count() ? 1 : 0;
+    if constexpr (NS == NSLOT) {
+        if (p.block_table) {
+            hipLaunchKernelGGL((prefill_kernel<TIN, TOUT, D, NS, CAUSAL, true>), dim3((unsigned)nblocks),
+                               dim3(SM::NT), 0, stream, a);
+            return hipGetLastError();
+        }
+    } else if (p.block_table) {
+        return hipErrorInvalidValue;   // paged K/V takes the default slots
+    }
+    hipLaunchKernelGGL((prefill_kernel<TIN, TOUT, D, NS, CAUSAL, false>), dim3((unsigned)nblocks),
+                       dim3(SM::NT), 0, stream, a);
     return hipGetLastError();
+}
+
+template <typename TIN, typename TOUT, int D, bool CAUSAL>
+hipError_t launch_s(const Problem &p, hipStream_t s) {
+    switch (p.slots) {
+    case 1: return launch_t<TIN, TOUT, D, 1, CAUSAL>(p, s);
+    case 2: return launch_t<TIN, TOUT, D, 2, CAUSAL>(p, s);
+    case 8: return launch_t<TIN, TOUT, D, 8, CAUSAL>(p, s);
+    default: return launch_t<TIN, TOUT, D, NSLOT, CAUSAL>(p, s);
+    }
 }
 
 template <typename TIN, typename TOUT>
 hipError_t launch_d(const Problem &p, hipStream_t s) {
-    if (p.D == 64) return p.causal ? launch_t<TIN, TOUT, 64, true>(p, s)
-                                   : launch_t<TIN, TOUT, 64, false>(p, s);
-    return p.causal ? launch_t<TIN, TOUT, 128, true>(p, s) : launch_t<TIN, TOUT, 128, false>(p, s);
+    if (p.D == 64) return p.causal ? launch_s<TIN, TOUT, 64, true>(p, s)
+                                   : launch_s<TIN, TOUT, 64, false>(p, s);
+    return p.causal ? launch_s<TIN, TOUT, 128, true>(p, s) : launch_s<TIN, TOUT, 128, false>(p, s);
 }
 
 }  // namespace

@@ -279,3 +279,20 @@ def test_noalloc_size_limit_before_any_launch():
     assert lib.fa_workspace_bytes(256, 64, 8, 1, 65536, 128, BF16, 16) > (32 << 20)
     assert lib.fa_fwd_splitkv_noalloc(*far, 256, 64, 8, 1, 65536, 128, 0, 0.088, None, BF16, BF16, 300) == 12
     assert lib.fa_fwd_splitkv_noalloc(None, *far[1:], 2, 8, 2, 1, 100, 64, 0, 0.1, None, BF16, BF16, 0) == 1
+
+
+def test_workgroup_layout_argument_errors():
+    """fa_fwd_slots: slots 0, 1, 2, 4, 8; heads 0, 1, 2, 4, 8 dividing Hq / Hkv
+    and the slots; anything else is FA_ERR_PACKING before any HIP call."""
+    lib = _lib.load()
+    Q, K, V, O, L = (k << 32 for k in range(1, 6))
+    F16 = _lib.FA_F16
+
+    def call(slots, heads, Hq=16, Hkv=2):
+        return lib.fa_fwd_slots(Q, K, V, O, L, 1, Hq, Hkv, 64, 64, 64, 1, 0.125, None, F16, F16, slots, heads)
+
+    for slots, heads in [(3, 0), (16, 0), (-1, 0), (4, 8), (2, 4), (1, 2), (8, 3), (8, 16)]:
+        assert call(slots, heads) == 13, (slots, heads)
+    assert call(8, 8, Hq=12, Hkv=3) == 13          # 8 heads do not divide the group of 4
+    assert call(4, 2, Hq=6, Hkv=2) == 13           # nor 2 a group of 3
+    assert lib.fa_fwd_packed(Q, K, V, O, L, 1, 16, 2, 64, 64, 64, 1, 0.125, None, F16, F16, 8) == 13

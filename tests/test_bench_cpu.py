@@ -33,3 +33,29 @@ def test_unfused_min_bytes_counts_each_array_once():
         2 * s_bytes + 2 * p_bytes + q_o + k_v
     # the headline workload: 12 x 67,141,632 visible scores + 20,971,520 bytes of Q, K, V, O
     assert bench.unfused_min_bytes(1, 32, 8, 2048, 2048, 64, 2048 * 2049 // 2, 2) == 826_671_104
+
+
+def test_staged_kv_bytes_brute_force():
+    """The packing ablation's staged K/V bytes: every workgroup (slots / heads
+    row blocks of 32 rows, `heads` query heads) stages each key tile its last
+    row reaches, K and V, counted here by enumerating rows and tiles."""
+    import math
+
+    for (B, Hq, Hkv, Nq, Nk, D, causal) in [(1, 8, 2, 100, 130, 64, True), (2, 16, 1, 70, 70, 128, True),
+                                            (1, 4, 4, 33, 90, 64, False)]:
+        w = Workload("t", B, Hq, Hkv, Nq, Nk, D, causal, "f16", 0)
+        bc = 64 if D == 64 else 32
+        G = Hq // Hkv
+        for slots, heads in [(1, 1), (2, 1), (4, 1), (4, 2), (8, 1)]:
+            if G % heads:
+                continue
+            rows = 32 * (slots // heads)
+            total = 0
+            for b in range(B):
+                for g in range(Hkv):
+                    for hg in range(G // heads):
+                        for r0 in range(0, Nq, rows):
+                            seen = max((min(Nk, i + Nk - Nq + 1) if causal else Nk)
+                                       for i in range(r0, min(r0 + rows, Nq)))
+                            total += math.ceil(seen / bc) * bc * D * 2 * 2
+            assert bench.staged_kv_bytes(w, slots, heads) == total, (B, Hq, Hkv, Nq, Nk, D, slots, heads)

@@ -87,6 +87,28 @@ def test_prefill_full_size_sampled_rows(name):
     assert torch.isfinite(o.float()).all()
 
 
+# Large D = 64 grids (more two-part workgroups than two per CU: the prefill
+# kernel's two-key-part layout), bf16 and fp16, causal with ragged rows and
+# keys and non-causal, sampled rows against the oracle.
+LARGE_D64 = [(2, 64, 8, 4100, 4100, True, "bf16"), (1, 32, 8, 3000, 3100, False, "bf16"),
+             (3, 16, 2, 2000, 2333, True, "f16")]
+
+
+@pytest.mark.parametrize("shape", LARGE_D64, ids=lambda s: "x".join(map(str, s)))
+def test_prefill_large_d64_grids_sampled_rows(shape):
+    B, Hq, Hkv, Nq, Nk, causal, dt = shape
+    q, k, v = make_qkv(B, Hq, Hkv, Nq, Nk, 64, dt, seed=zlib.crc32(repr(shape).encode()))
+    scale = default_scale(64)
+    rows = sample_rows(B, Hq, Nq, 160, seed=7)
+    o_r, l_r = oracle.attention_rows(q, k, v, causal, scale, rows, workers=oracle.default_workers())
+    for verify in (True, False):
+        o, lse = gpu_attention(q, k, v, causal, scale, out_dtype=torch.float32 if verify else None)
+        b_i, h_i, q_i = (torch.from_numpy(rows[:, j]).long().to(o.device) for j in range(3))
+        check_against(o[b_i, q_i, h_i].cpu(), lse[b_i, h_i, q_i].cpu(), o_r, l_r, DTYPES[dt], verify,
+                      f"large D=64 {shape} verify={verify}")
+    assert torch.isfinite(o.float()).all()
+
+
 @pytest.mark.parametrize("name", ["gqa_prefill_bf16", "gqa_prefill_d128_f16", "mqa_prefill_f16"])
 def test_prefill_full_size_every_element(name):
     """Every output element and lse of the three prefill workloads at full
@@ -262,29 +284,66 @@ def test_caller_owned_workspace():
     check_against(o_usr, l_usr, o_ref, l_ref, DTYPES["bf16"], True, "caller workspace")
 
 
+def _layouts(G):
+    """Every (slots, heads) workgroup layout fa_fwd_slots takes for group size G."""
+    return [(s, h) for s in (1, 2, 4, 8) for h in (1, 2, 4, 8) if h <= s and s % h == 0 and G % h == 0]
+
+
+@pytest.mark.parametrize("full", [False, True], ids=["reduced", "full_size"])
 @pytest.mark.parametrize("name", ["gqa_prefill_bf16", "gqa_prefill_d128_f16", "mqa_prefill_f16"])
-def test_head_packing_schedules_agree_bitwise(name):
-    """The inter-head packing (query heads of one K/V group sharing a
-    workgroup's K/V tiles) against the per-head schedule and the 2-head one:
-    every row's arithmetic is the same, so the outputs agree bit for bit, and
-    the per-head schedule matches the oracle."""
-    w = shrink(WORKLOADS[name], **REDUCED[name])
+def test_head_packing_schedules_agree_bitwise(name, full):
+    """Every workgroup layout -- 1, 2, 4 or 8 query slots sharing each staged
+    K/V tile, 1 to 8 of them query heads of one K/V group (the inter-head
+    packing) -- against the default one: every row's arithmetic is the same,
+    so the outputs agree bit for bit (as shipped and in verify mode), and the
+    unshared one-slot layout matches the oracle on the reduced shapes."""
+    w = WORKLOADS[name] if full else shrink(WORKLOADS[name], **REDUCED[name])
     q, k, v = make_workload(w)
     qd, kd, vd = (t.cuda() for t in (q, k, v))
     G = w.Hq // w.Hkv
-    outs = {}
-    for hw in (4, 2, 1):
-        if G % hw:
-            continue
-        o, lse = fa.fwd(qd, kd, vd, causal=w.causal, scale=w.softmax_scale, out_dtype=torch.float32,
-                        heads_per_workgroup=hw)
+    for odt in (torch.float32, None):
+        ref_o, ref_l = fa.fwd(qd, kd, vd, causal=w.causal, scale=w.softmax_scale, out_dtype=odt)
         torch.cuda.synchronize()
-        outs[hw] = (o, lse)
-    ref_o, ref_l = outs[max(outs)]
-    for hw, (o, lse) in outs.items():
-        assert torch.equal(o, ref_o) and torch.equal(lse, ref_l), f"packing {hw}"
-    o_ref, l_ref = oracle_full(q, k, v, w.causal, w.softmax_scale)
-    check_against(outs[1][0], outs[1][1], o_ref, l_ref, DTYPES[w.dtype], True, f"{name} per-head")
+        outs = {}
+        for slots, hw in _layouts(G):
+            o, lse = fa.fwd(qd, kd, vd, causal=w.causal, scale=w.softmax_scale, out_dtype=odt,
+                            slots_per_workgroup=slots, heads_per_workgroup=hw)
+            torch.cuda.synchronize()
+            assert torch.equal(o, ref_o) and torch.equal(lse, ref_l), f"{slots} slots, {hw} heads"
+            outs[(slots, hw)] = (o, lse)
+        for hw in (1, 2, 4):   # fa_fwd_packed: the default four slots
+            if G % hw == 0:
+                o, lse = fa.fwd(qd, kd, vd, causal=w.causal, scale=w.softmax_scale, out_dtype=odt,
+                                heads_per_workgroup=hw)
+                torch.cuda.synchronize()
+                assert torch.equal(o, ref_o) and torch.equal(lse, ref_l), f"packed {hw}"
+        if odt is torch.float32 and not full:
+            o_ref, l_ref = oracle_full(q, k, v, w.causal, w.softmax_scale)
+            check_against(outs[(1, 1)][0], outs[(1, 1)][1], o_ref, l_ref, DTYPES[w.dtype], True,
+                          f"{name} one slot")
+
+
+@pytest.mark.parametrize("shape", [(1, 16, 2, 70, 70, 64, 1, "bf16"), (2, 6, 3, 100, 130, 128, 1, "f16"),
+                                   (1, 16, 1, 45, 200, 64, 0, "f16"), (1, 8, 8, 33, 33, 128, 1, "bf16")],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_workgroup_layouts_against_oracle(shape):
+    """The one-, two- and eight-slot layouts on ragged rows and keys, causal
+    with Nq < Nk and MHA, each against the oracle (as shipped and in verify
+    mode)."""
+    B, Hq, Hkv, Nq, Nk, D, causal, dt = shape
+    q, k, v = make_qkv(B, Hq, Hkv, Nq, Nk, D, dt, seed=zlib.crc32(repr(shape).encode()))
+    scale = default_scale(D)
+    o_ref, l_ref = oracle.attention(q, k, v, bool(causal), scale)
+    qd, kd, vd = (t.cuda() for t in (q, k, v))
+    for slots, hw in _layouts(Hq // Hkv):
+        if slots == 4:
+            continue
+        for verify in (True, False):
+            o, lse = fa.fwd(qd, kd, vd, causal=bool(causal), scale=scale,
+                            out_dtype=torch.float32 if verify else None,
+                            slots_per_workgroup=slots, heads_per_workgroup=hw)
+            torch.cuda.synchronize()
+            check_against(o, lse, o_ref, l_ref, DTYPES[dt], verify, f"{shape} {slots} slots {hw} heads")
 
 
 def _kvcache_check(q, k, v, seqlens, causal, scale, dt, label):
