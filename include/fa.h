@@ -134,13 +134,16 @@ fa_status_t fa_fwd_splitkv(const void *q, const void *k, const void *v, void *o,
                            fa_dtype_t out_dtype, int num_splits);
 
 /* Prefill with an explicit query-head packing (the inter-head packing of
- * Sec. 4.1.1 and the GQA K/V reuse of Sec. 4.1.2 (iv)).  A prefill workgroup
- * owns four 32-row query slots that read one key/value head;
+ * Sec. 4.1.1 and the GQA K/V reuse of Sec. 4.1.2 (iv)).  With a nonzero
+ * heads_per_workgroup a prefill workgroup owns four 32-row query slots that
+ * read one key/value head;
  * heads_per_workgroup of them are different query heads of that key/value
  * group (at the same rows), so each K/V tile staged in LDS serves that many
  * heads, and the rest are consecutive row blocks.  1 is the per-head
- * schedule (four consecutive row blocks of one head); 0 picks what fa_fwd
- * uses (4 when 4 divides Hq / Hkv, else 2 when 2 does, else 1).  The result
+ * schedule (four consecutive row blocks of one head); 0 does what fa_fwd
+ * does (fa_fwd_slots with 0, 0: at D = 64 on a large grid eight slots, and
+ * otherwise four, with 4 heads when 4 divides Hq / Hkv, else 2 when 2 does,
+ * else 1).  The result
  * is the same, bit for bit, for every packing.  Only the fp16 / bf16 prefill
  * kernels (Nq > 1, D in {64, 128}) take the packing; other calls ignore it.
  * Errors: FA_ERR_PACKING for a value other than 0, 1, 2, 4 or one that does
@@ -157,8 +160,11 @@ fa_status_t fa_fwd_packed(const void *q, const void *k, const void *v, void *o, 
  * slots (the reuse the inter-head packing of Sec. 4.1.1 and Fig. 1 is about:
  * one load of a key/value row serving several query heads), and
  * heads_per_workgroup of them are different query heads of the group (the
- * rest consecutive row blocks).  slots_per_workgroup: 0 (the default, 4), 1
- * (no sharing: every slot stages its own tiles), 2, 4 or 8;
+ * rest consecutive row blocks).  slots_per_workgroup: 0 (what fa_fwd uses:
+ * 8 at D = 64 when that still gives every compute unit two or more
+ * workgroups, the K/V is contiguous and heads_per_workgroup is 0; else 4),
+ * 1 (no sharing: every slot
+ * stages its own tiles), 2, 4 or 8;
  * heads_per_workgroup: 0 (the most heads, up to 4, that divide both the slots
  * and Hq / Hkv), 1, 2, 4 or 8, dividing Hq / Hkv and the slots.  The result
  * is the same, bit for bit, for every layout.  Only the fp16 / bf16 prefill

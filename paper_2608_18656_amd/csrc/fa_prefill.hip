@@ -75,12 +75,13 @@ struct PrefillArgs {
 // CU (three waves per SIMD, from independent workgroups; operands are read
 // from LDS in small groups to fit 168 VGPRs).  Two LDS stages in both.
 // NS, the slots per workgroup (all reading one key/value head, each staged
-// tile serving all of them), is 4 by default; 1, 2 and 8 exist for the
-// packing ablation (fewer slots stage more per thread, so they hold fewer
-// waves per SIMD).
+// tile serving all of them), is 4 or, at D = 64 on large grids, 8; 1 and 2
+// exist for the packing ablation (fewer slots stage more per thread, so they
+// hold fewer waves per SIMD).
 template <int D, int NS = NSLOT> struct Cfg {
     static constexpr int NQ = D == 64 ? 2 : 1;       // waves per slot
-    static constexpr int WPE = D == 64 ? (NS >= 4 ? 4 : 3) : (NS >= 4 ? 3 : 2);   // waves per SIMD
+    // waves per SIMD (what the registers allow; fewer slots stage more per thread)
+    static constexpr int WPE = D == 64 ? (NS >= 4 ? 4 : NS == 2 ? 3 : 2) : (NS >= 4 ? 3 : NS == 2 ? 2 : 1);
     static constexpr int NWG = NS * NQ;              // waves per workgroup
     static constexpr int WPC = NWG >= 4 * WPE ? 1 : 4 * WPE / NWG;   // workgroups per CU (registers)
     static constexpr int BC = 32 * NQ;               // keys per tile
@@ -660,9 +661,26 @@ hipError_t launch_t(const Problem &p, hipStream_t stream) {
     return hipGetLastError();
 }
 
+// Default slots per workgroup: 8 at D = 64 when the grid of 8-slot workgroups
+// (the default heads, up to 4, times 2 row blocks) still gives every CU at
+// least two of them -- each staged tile then serves twice the rows (MQA
+// prefill, 16 heads on one K/V head, 16384 rows: 578 against 602 us); 4
+// otherwise (a small grid, e.g. the 32-head, 2048-row GQA prefill, needs the
+// smaller workgroups: 39 against 31.5 us), for paged K/V and when the caller
+// fixed the heads per workgroup.
+int default_slots(const Problem &p) {
+    if (p.D != 64 || p.block_table || p.hw > 0) return NSLOT;
+    const int G = p.Hq / p.Hkv;
+    const int hw = G % 4 == 0 ? 4 : G % 2 == 0 ? 2 : 1;
+    const int rows = WR * (8 / hw);
+    const long long nblocks = (long long)((p.Nq + rows - 1) / rows) * p.B * p.Hkv * (G / hw);
+    const int cus = cu_count();
+    return cus > 0 && nblocks >= 2LL * cus ? 8 : NSLOT;
+}
+
 template <typename TIN, typename TOUT, int D, bool CAUSAL>
 hipError_t launch_s(const Problem &p, hipStream_t s) {
-    switch (p.slots) {
+    switch (p.slots > 0 ? p.slots : default_slots(p)) {
     case 1: return launch_t<TIN, TOUT, D, 1, CAUSAL>(p, s);
     case 2: return launch_t<TIN, TOUT, D, 2, CAUSAL>(p, s);
     case 8: return launch_t<TIN, TOUT, D, 8, CAUSAL>(p, s);

@@ -374,6 +374,8 @@ def _kvcache_check(q, k, v, seqlens, causal, scale, dt, label):
     # chunked prefill: Nq new tokens at the end of each sequence
     (3, 8, 2, 70, 600, 64, "f16", True, [600, 70, 333]),
     (2, 32, 8, 64, 512, 128, "bf16", True, [512, 200]),
+    # a D = 64 grid large enough for the default eight-slot workgroups
+    (4, 64, 8, 512, 1200, 64, "bf16", True, [1200, 512, 700, 1000]),
     # a chunk longer than its sequence: the first rows see no key
     (2, 4, 4, 100, 256, 128, "bf16", True, [40, 256]),
     # the vector-ALU kernel (fp32)
@@ -387,7 +389,8 @@ def test_kvcache_per_sequence_lengths(case):
 
 @pytest.mark.parametrize("shape", [(2, 32, 8, 1, 2000, 128, "bf16", False),
                                    (1, 32, 8, 333, 333, 64, "bf16", True),
-                                   (1, 16, 1, 200, 260, 64, "f16", True)])
+                                   (1, 16, 1, 200, 260, 64, "f16", True),
+                                   (4, 64, 8, 600, 600, 64, "f16", True)])
 def test_kvcache_full_lengths_equal_fa_fwd_bitwise(shape):
     B, Hq, Hkv, Nq, Nk, D, dt, causal = shape
     q, k, v = make_qkv(B, Hq, Hkv, Nq, Nk, D, dt, seed=950 + Nq)
