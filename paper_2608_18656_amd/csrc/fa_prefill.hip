@@ -1,14 +1,16 @@
 // fa_prefill.hip -- prefill attention forward on gfx950 matrix cores.
 //
-// Work split.  A workgroup owns four (query head, 32-row block) slots that
-// read the same key/value head.  When the group size G = Hq/Hkv allows, the
-// four slots are four query heads of one key/value group at the same rows --
-// the GPU form of the inter-head packing of Sec. 4.1.1 and the GQA reuse of
-// Sec. 4.1.2 (iv): every K/V tile staged in LDS serves four heads, and all
-// slots share one causal extent.  Otherwise (G = 1 or odd) the slots are
-// consecutive row blocks of one head.  Every wave handles 32 rows and 32 keys
-// of each tile.  At D = 64 a slot has two waves (64-key tiles; wave kh takes
-// keys 32 kh .. 32 kh + 31) whose states are merged through LDS at the end; at
+// Work split.  A workgroup owns NS (query head, 32-row block) slots that read
+// the same key/value head: four, or eight on grids large enough to give every
+// CU two or more eight-slot workgroups (1 and 2 exist for the packing
+// ablation).  When the group size G = Hq/Hkv allows, up to four of the slots
+// are query heads of one key/value group at the same rows -- the GPU form of
+// the inter-head packing of Sec. 4.1.1 and the GQA reuse of Sec. 4.1.2 (iv):
+// every K/V tile staged in LDS serves all slots of the workgroup, and slots
+// of different heads share one causal extent; the other slots are
+// consecutive row blocks.  Every wave handles 32 rows and 32 keys of each
+// tile.  At D = 64 a slot has two waves (64-key tiles; wave kh takes keys
+// 32 kh .. 32 kh + 31) whose states are merged through LDS at the end; at
 // D = 128 one wave (32-key tiles).
 //
 // Per wave and tile, the blocked streaming softmax (Alg. 2 state carry over
@@ -29,11 +31,11 @@
 // grow too large (see the softmax step below), so the accumulator rescale is
 // skipped on most tiles; sum and accumulator always share the base, so the
 // result is unchanged.
-// A wave's steps run in order; latency is hidden by running several
-// workgroups per CU (two 8-wave ones at D = 64: four waves per SIMD within 128
-// VGPRs; three 4-wave ones at D = 128: three waves per SIMD within 168 VGPRs),
-// whose barriers are independent.  Matrix instructions are issued at raised
-// wave priority.
+// A wave's steps run in order; latency is hidden by the other waves of the
+// SIMD (four-slot layouts: two 8-wave workgroups per CU at D = 64, four waves
+// per SIMD within 128 VGPRs; three 4-wave ones at D = 128, three waves per
+// SIMD within 168 VGPRs; their barriers are independent).  Matrix
+// instructions are issued at raised wave priority.
 // Masked scores are -inf and give exactly 0 (the exponent factor is kept
 // strictly positive, also for scale = 0).  Keys past the end read as zero
 // (buffer loads with the tensor's extent as the range) and are masked.
