@@ -139,7 +139,7 @@ def loaded_sclk_mhz(torch, call, seconds=2.0):
 # workgroup, query heads among them).  Every staged K/V tile serves all slots
 # of its workgroup: one slot (no sharing), four row blocks of one head, four
 # heads of one K/V group (the default for small grids), eight slots of four
-# heads (the default for large grids), eight heads of an MQA group.
+# heads (the default for large D = 64 grids), eight heads of an MQA group.
 LAYOUTS = {
     "gqa_prefill_bf16": [("unshared", 1, 1), ("per_head", 4, 1), ("packed", 4, 4)],
     "gqa_prefill_d128_f16": [("unshared", 1, 1), ("per_head", 4, 1), ("packed", 4, 4), ("eight_slots", 8, 4)],

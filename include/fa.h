@@ -141,8 +141,8 @@ fa_status_t fa_fwd_splitkv(const void *q, const void *k, const void *v, void *o,
  * group (at the same rows), so each K/V tile staged in LDS serves that many
  * heads, and the rest are consecutive row blocks.  1 is the per-head
  * schedule (four consecutive row blocks of one head); 0 does what fa_fwd
- * does (fa_fwd_slots with 0, 0: on a large grid eight slots, and otherwise
- * four, with 4 heads when 4 divides Hq / Hkv, else 2 when 2 does,
+ * does (fa_fwd_slots with 0, 0: at D = 64 on a large grid eight slots, and
+ * otherwise four, with 4 heads when 4 divides Hq / Hkv, else 2 when 2 does,
  * else 1).  The result
  * is the same, bit for bit, for every packing.  Only the fp16 / bf16 prefill
  * kernels (Nq > 1, D in {64, 128}) take the packing; other calls ignore it.
@@ -161,8 +161,8 @@ fa_status_t fa_fwd_packed(const void *q, const void *k, const void *v, void *o, 
  * one load of a key/value row serving several query heads), and
  * heads_per_workgroup of them are different query heads of the group (the
  * rest consecutive row blocks).  slots_per_workgroup: 0 (what fa_fwd uses:
- * 8 when that still gives every compute unit two or more workgroups, the
- * K/V is contiguous and heads_per_workgroup is 0; else 4),
+ * 8 at D = 64 when that still gives every compute unit two or more
+ * workgroups, the K/V is contiguous and heads_per_workgroup is 0; else 4),
  * 1 (no sharing: every slot
  * stages its own tiles), 2, 4 or 8;
  * heads_per_workgroup: 0 (the most heads, up to 4, that divide both the slots

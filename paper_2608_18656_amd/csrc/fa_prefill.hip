@@ -1,9 +1,9 @@
 // fa_prefill.hip -- prefill attention forward on gfx950 matrix cores.
 //
 // Work split.  A workgroup owns NS (query head, 32-row block) slots that read
-// the same key/value head: four, or eight on grids large enough to give every
-// CU two or more eight-slot workgroups (1 and 2 exist for the packing
-// ablation).  When the group size G = Hq/Hkv allows, up to four of the slots
+// the same key/value head: four, or at D = 64 eight on grids large enough to
+// give every CU two or more eight-slot workgroups (1 and 2 exist for the
+// packing ablation).  When the group size G = Hq/Hkv allows, up to four of the slots
 // are query heads of one key/value group at the same rows -- the GPU form of
 // the inter-head packing of Sec. 4.1.1 and the GQA reuse of Sec. 4.1.2 (iv):
 // every K/V tile staged in LDS serves all slots of the workgroup, and slots
@@ -77,8 +77,8 @@ struct PrefillArgs {
 // CU (three waves per SIMD, from independent workgroups; operands are read
 // from LDS in small groups to fit 168 VGPRs).  Two LDS stages in both.
 // NS, the slots per workgroup (all reading one key/value head, each staged
-// tile serving all of them), is 4 or, on large grids, 8; 1 and 2 exist for
-// the packing ablation (fewer slots stage more per thread, so they
+// tile serving all of them), is 4 or, at D = 64 on large grids, 8; 1 and 2
+// exist for the packing ablation (fewer slots stage more per thread, so they
 // hold fewer waves per SIMD).
 template <int D, int NS = NSLOT> struct Cfg {
     static constexpr int NQ = D == 64 ? 2 : 1;       // waves per slot
@@ -663,16 +663,17 @@ hipError_t launch_t(const Problem &p, hipStream_t stream) {
     return hipGetLastError();
 }
 
-// Default slots per workgroup: 8 when the grid of 8-slot workgroups (the
-// default heads, up to 4, times 2 row blocks) still gives every CU at least
-// two of them -- each staged tile then serves twice the rows (MQA prefill at
-// D = 64, 16 heads on one K/V head, 16384 rows: 578 against 602 us; the
-// 32-head, 4096-row D = 128 prefill: 288 against 295 us); 4 otherwise (a
-// small grid, e.g. the 32-head, 2048-row GQA prefill, needs the smaller
-// workgroups: 39 against 31.5 us), for paged K/V and when the caller fixed
-// the heads per workgroup.
+// Default slots per workgroup: 8 at D = 64 when the grid of 8-slot
+// workgroups (the default heads, up to 4, times 2 row blocks) still gives
+// every CU at least two of them -- each staged tile then serves twice the
+// rows (MQA prefill, 16 heads on one K/V head, 16384 rows: 578 against
+// 602 us); 4 otherwise: on a small grid (the 32-head, 2048-row GQA prefill:
+// 39 against 31.5 us), at D = 128 (the eight-slot workgroup holds two waves
+// per SIMD instead of three; on the 32-head, 4096-row prefill it ran from
+// 2 % faster to 3 % slower depending on the box), for paged K/V and when the
+// caller fixed the heads per workgroup.
 int default_slots(const Problem &p) {
-    if (p.block_table || p.hw > 0) return NSLOT;
+    if (p.D != 64 || p.block_table || p.hw > 0) return NSLOT;
     const int G = p.Hq / p.Hkv;
     const int hw = G % 4 == 0 ? 4 : G % 2 == 0 ? 2 : 1;
     const int rows = WR * (8 / hw);

@@ -374,7 +374,7 @@ def _kvcache_check(q, k, v, seqlens, causal, scale, dt, label):
     # chunked prefill: Nq new tokens at the end of each sequence
     (3, 8, 2, 70, 600, 64, "f16", True, [600, 70, 333]),
     (2, 32, 8, 64, 512, 128, "bf16", True, [512, 200]),
-    # grids large enough for the default eight-slot workgroups
+    # grids large enough for eight-slot workgroups (the default at D = 64)
     (4, 64, 8, 512, 1200, 64, "bf16", True, [1200, 512, 700, 1000]),
     (4, 64, 8, 512, 1100, 128, "f16", True, [1100, 512, 640, 900]),
     # a chunk longer than its sequence: the first rows see no key
