@@ -376,6 +376,7 @@ def _kvcache_check(q, k, v, seqlens, causal, scale, dt, label):
     (2, 32, 8, 64, 512, 128, "bf16", True, [512, 200]),
     # grids large enough for eight-slot workgroups (the default at D = 64)
     (4, 64, 8, 512, 1200, 64, "bf16", True, [1200, 512, 700, 1000]),
+    (4, 64, 8, 512, 1200, 64, "f16", True, [1200, 0, 700, 37]),   # and keyless rows
     (4, 64, 8, 512, 1100, 128, "f16", True, [1100, 512, 640, 900]),
     # a chunk longer than its sequence: the first rows see no key
     (2, 4, 4, 100, 256, 128, "bf16", True, [40, 256]),
