@@ -59,3 +59,18 @@ def test_staged_kv_bytes_brute_force():
                                        for i in range(r0, min(r0 + rows, Nq)))
                             total += math.ceil(seen / bc) * bc * D * 2 * 2
             assert bench.staged_kv_bytes(w, slots, heads) == total, (B, Hq, Hkv, Nq, Nk, D, slots, heads)
+
+
+def test_more_than_one_gpu_is_refused_with_a_message():
+    """The benchmark measures one GPU: --gpus above 1 (or a WORLD_SIZE above 1)
+    exits with status 2 and says so, before touching a GPU."""
+    import os
+    import subprocess
+    import sys
+
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    for args, env in [(["--gpus", "2"], {}), ([], {"WORLD_SIZE": "4"})]:
+        r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), *args], capture_output=True, text=True,
+                           env={**os.environ, **env}, timeout=120)
+        assert r.returncode == 2, (args, env, r.returncode)
+        assert "one GPU" in r.stderr, r.stderr
